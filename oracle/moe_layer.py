@@ -271,25 +271,50 @@ def token_forward_backward(inp, tokens, dy_rows=None):
     """Y (and, with dY given, dgate and the expert part of dX) for a subset of tokens.
 
     Each token's routed experts and the shared experts are evaluated on that token's row
-    alone, exactly as the whole-layer definition does for it."""
+    alone, exactly as the whole-layer definition does for it (grouped by expert so that each
+    expert's weights are converted once)."""
     cfg = inp.cfg
     Eloc, S, k = cfg.n_local, cfg.n_shared, cfg.k
+    tokens = np.asarray(tokens)
     _, L32, idx, w = token_route(inp, tokens)
     x = f64(inp.x[tokens])
-    Y = np.zeros((len(tokens), cfg.d))
-    dgate = np.zeros((len(tokens), k))
-    dx = np.zeros((len(tokens), cfg.d))
-    for i in range(len(tokens)):
-        h = x[i:i + 1]
-        exps = [(int(idx[i, j]) - cfg.local_begin, w[i, j], j) for j in range(k)]
-        exps = [(g, wj, j) for (g, wj, j) in exps if 0 <= g < Eloc] + [(Eloc + s, 1.0, None) for s in range(S)]
-        for g, wj, j in exps:
-            G, U, Hd, O = expert_forward(h, inp.w_gate[g], inp.w_up[g], inp.w_down[g])
-            Y[i] += wj * O[0]
-            if dy_rows is not None:
-                dyi = f64(dy_rows[i:i + 1])
-                b = expert_backward(h, inp.w_gate[g], inp.w_up[g], inp.w_down[g], G, U, Hd, wj * dyi)
-                dx[i] += b["dh"][0]
-                if j is not None:
-                    dgate[i, j] = float((dyi * O).sum())
+    n = len(tokens)
+    Y = np.zeros((n, cfg.d))
+    dgate = np.zeros((n, k))
+    dx = np.zeros((n, cfg.d))
+    dyr = None if dy_rows is None else f64(dy_rows)
+    for g in range(Eloc + S):
+        if g < Eloc:
+            hit = np.argwhere(idx == cfg.local_begin + g)      # (token position, slot j)
+            if hit.size == 0:
+                continue
+            rows, slots = hit[:, 0], hit[:, 1]
+            wj = w[rows, slots][:, None]
+        else:
+            rows, slots = np.arange(n), None
+            wj = np.ones((n, 1))
+        G, U, Hd, O = expert_forward(x[rows], inp.w_gate[g], inp.w_up[g], inp.w_down[g])
+        np.add.at(Y, rows, wj * O)
+        if dyr is not None:
+            b = expert_backward(x[rows], inp.w_gate[g], inp.w_up[g], inp.w_down[g], G, U, Hd, wj * dyr[rows])
+            np.add.at(dx, rows, b["dh"])
+            if slots is not None:
+                dgate[rows, slots] = (dyr[rows] * O).sum(axis=1)
     return dict(y=Y, dgate=dgate, dx_experts=dx, topk_idx=idx, topk_w=w, logits=L32)
+
+
+def expert_wgrad_slices(h, dO, w_gate, w_up, w_down, rows_ff, cols_ff):
+    """Selected rows of dW_gate / dW_up (inner units rows_ff) and columns of dW_down (inner units
+    cols_ff) of one expert, without forming its full backward: each needs only the inner units
+    it names (Alg. 6 backward restricted to those units)."""
+    h, dO = f64(h), f64(dO)
+    wg, wu, wd = f64(w_gate), f64(w_up), f64(w_down)
+    rows_ff, cols_ff = np.asarray(rows_ff), np.asarray(cols_ff)
+    G = h @ wg[rows_ff].T
+    U = h @ wu[rows_ff].T
+    dHid = dO @ wd[:, rows_ff]
+    dG = dHid * U * dsilu(G)
+    dU = dHid * silu(G)
+    Gc = h @ wg[cols_ff].T
+    Hc = silu(Gc) * (h @ wu[cols_ff].T)
+    return dict(dW_gate_rows=dG.T @ h, dW_up_rows=dU.T @ h, dW_down_cols=dO.T @ Hc)

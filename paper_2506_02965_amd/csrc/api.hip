@@ -1,0 +1,285 @@
+// C ABI of the pcmoe library: argument validation (before any HIP call), workspace sizing,
+// error reporting and the optional per-kernel event timing. Kernels live in the other files.
+#include "pcmoe_internal.h"
+
+#include <mutex>
+#include <string>
+#include <vector>
+#include <map>
+#include <cstdio>
+#include <cstring>
+#include <cstdarg>
+
+using namespace pcmoe;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+moe_status fail(moe_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+moe_status fail(moe_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+moe_status hip_status(hipError_t e, const char* where) {
+  if (e == hipSuccess) return MOE_OK;
+  return fail(MOE_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+moe_status check_desc(const moe_desc* d) {
+  if (!d) return fail(MOE_ERR_INVALID_ARGUMENT, "desc is NULL");
+  if (d->dtype != MOE_F32 && d->dtype != MOE_BF16) return fail(MOE_ERR_INVALID_ARGUMENT, "dtype %d", d->dtype);
+  if (d->T < 1 || d->d_model < 1 || d->d_ff < 1 || d->n_experts < 1)
+    return fail(MOE_ERR_INVALID_ARGUMENT, "non-positive shape T=%d d=%d f=%d E=%d", d->T, d->d_model, d->d_ff,
+                d->n_experts);
+  if (d->top_k < 1 || d->top_k > d->n_experts)
+    return fail(MOE_ERR_INVALID_ARGUMENT, "top_k=%d outside [1, E=%d]", d->top_k, d->n_experts);
+  if (d->local_count < 0 || d->local_begin < 0 || d->local_begin + d->local_count > d->n_experts)
+    return fail(MOE_ERR_INVALID_ARGUMENT, "hosted range [%d, %d+%d) outside [0, %d)", d->local_begin,
+                d->local_begin, d->local_count, d->n_experts);
+  if (d->local_count + d->n_shared < 1 || d->n_shared < 0)
+    return fail(MOE_ERR_INVALID_ARGUMENT, "no expert to compute (local_count=%d n_shared=%d)", d->local_count,
+                d->n_shared);
+  if (d->renormalize != 0 && d->renormalize != 1)
+    return fail(MOE_ERR_INVALID_ARGUMENT, "renormalize must be 0 or 1");
+  if (d->top_k > 8) return fail(MOE_ERR_UNSUPPORTED, "top_k=%d > 8", d->top_k);
+  if (d->n_experts > 256) return fail(MOE_ERR_UNSUPPORTED, "n_experts=%d > 256", d->n_experts);
+  if (d->local_count + d->n_shared > 511)
+    return fail(MOE_ERR_UNSUPPORTED, "local_count + n_shared = %d > 511", d->local_count + d->n_shared);
+  if (d->d_model % 128 || d->d_ff % 128)
+    return fail(MOE_ERR_UNSUPPORTED, "d_model=%d and d_ff=%d must be multiples of 128", d->d_model, d->d_ff);
+  const int64_t R = rows_total(*d);
+  if (R * (int64_t)(2 * d->d_ff) >= (int64_t)1 << 40 || R >= ((int64_t)1 << 31) / 2)
+    return fail(MOE_ERR_UNSUPPORTED, "row space of %lld rows is too large", (long long)R);
+  if ((int64_t)d->T * d->top_k >= ((int64_t)1 << 31) - 1024)
+    return fail(MOE_ERR_UNSUPPORTED, "T*k too large for int32 slot indices");
+  return MOE_OK;
+}
+
+#define NEED(p)                                                   \
+  do {                                                            \
+    if (!(p)) return fail(MOE_ERR_INVALID_ARGUMENT, #p " is NULL"); \
+  } while (0)
+
+#define NEED_WS(have, need)                                                                                   \
+  do {                                                                                                        \
+    size_t need_ = (need);                                                                                    \
+    if ((have) < need_)                                                                                       \
+      return fail(MOE_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes, %zu needed", (size_t)(have), need_); \
+    if (need_ && !ws) return fail(MOE_ERR_INVALID_ARGUMENT, "ws is NULL");                                    \
+  } while (0)
+
+// ------------------------------------------------------------------ per-kernel timing
+struct TimingState {
+  std::mutex mu;
+  bool on = false;
+  struct Rec {
+    std::string name;
+    hipEvent_t a, b;
+  };
+  std::vector<Rec> recs;
+  std::vector<hipEvent_t> pool;
+};
+TimingState& timing() {
+  static TimingState* t = new TimingState();
+  return *t;
+}
+
+}  // namespace
+
+namespace pcmoe {
+KernelTimer::KernelTimer(const char* n, hipStream_t s) : name(n), stream(s), slot(nullptr) {
+  TimingState& ts = timing();
+  std::lock_guard<std::mutex> lk(ts.mu);
+  if (!ts.on) return;
+  hipEvent_t a = nullptr, b = nullptr;
+  if (ts.pool.size() >= 2) {
+    a = ts.pool.back(); ts.pool.pop_back();
+    b = ts.pool.back(); ts.pool.pop_back();
+  } else {
+    if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) return;
+  }
+  hipEventRecord(a, s);
+  ts.recs.push_back({std::string(n), a, b});
+  slot = (void*)(uintptr_t)ts.recs.size();
+}
+KernelTimer::~KernelTimer() {
+  if (!slot) return;
+  TimingState& ts = timing();
+  std::lock_guard<std::mutex> lk(ts.mu);
+  size_t i = (size_t)(uintptr_t)slot - 1;
+  if (i < ts.recs.size()) hipEventRecord(ts.recs[i].b, stream);
+}
+}  // namespace pcmoe
+
+extern "C" {
+
+const char* moe_status_string(moe_status s) {
+  switch (s) {
+    case MOE_OK: return "MOE_OK";
+    case MOE_ERR_INVALID_ARGUMENT: return "MOE_ERR_INVALID_ARGUMENT";
+    case MOE_ERR_UNSUPPORTED: return "MOE_ERR_UNSUPPORTED";
+    case MOE_ERR_WORKSPACE_TOO_SMALL: return "MOE_ERR_WORKSPACE_TOO_SMALL";
+    case MOE_ERR_HIP: return "MOE_ERR_HIP";
+  }
+  return "MOE_ERR_UNKNOWN";
+}
+
+const char* moe_last_error(void) { return g_last_error.c_str(); }
+
+size_t moe_workspace_size(const moe_desc* d, int which) {
+  if (check_desc(d) != MOE_OK) return 0;
+  switch (which) {
+    case MOE_WS_PERMUTE: return permute_ws_bytes(*d);
+    case MOE_WS_FFN_SAVED: return ffn_saved_bytes(*d);
+    case MOE_WS_FFN_FWD: return ffn_fwd_ws_bytes(*d);
+    case MOE_WS_FFN_BWD: return ffn_bwd_ws_bytes(*d);
+    case MOE_WS_ROUTE_BWD: return route_bwd_ws_bytes(*d);
+  }
+  return 0;
+}
+
+moe_status moe_route(const moe_desc* d, const void* x, const void* w_router, const float* logit_bias,
+                     int32_t bias_groups, float* logits, int32_t* topk_idx, float* topk_w, hipStream_t stream) {
+  moe_status st = check_desc(d);
+  if (st) return st;
+  NEED(x); NEED(w_router); NEED(logits); NEED(topk_idx); NEED(topk_w);
+  if (logit_bias && (bias_groups < 1 || d->T % bias_groups))
+    return fail(MOE_ERR_INVALID_ARGUMENT, "bias_groups=%d must divide T=%d", bias_groups, d->T);
+  return hip_status(launch_route_fwd(*d, x, w_router, logit_bias, logit_bias ? bias_groups : 1, logits, topk_idx,
+                                     topk_w, stream),
+                    "moe_route");
+}
+
+moe_status moe_permute(const moe_desc* d, const int32_t* topk_idx, const void* x, int32_t* counts, int32_t* offsets,
+                       int32_t* row_to_slot, int32_t* slot_to_row, void* x_perm, void* ws, size_t ws_bytes,
+                       hipStream_t stream) {
+  moe_status st = check_desc(d);
+  if (st) return st;
+  if (d->local_count < 1) return fail(MOE_ERR_INVALID_ARGUMENT, "moe_permute needs local_count >= 1");
+  NEED(topk_idx); NEED(x); NEED(counts); NEED(offsets); NEED(row_to_slot); NEED(slot_to_row); NEED(x_perm);
+  NEED_WS(ws_bytes, permute_ws_bytes(*d));
+  return hip_status(launch_permute(*d, topk_idx, x, counts, offsets, row_to_slot, slot_to_row, x_perm, ws, stream),
+                    "moe_permute");
+}
+
+moe_status moe_expert_ffn_fwd(const moe_desc* d, const void* x, const void* x_perm, const int32_t* offsets,
+                              const void* w_gate, const void* w_up, const void* w_down, void* y_perm, void* saved,
+                              void* ws, size_t ws_bytes, hipStream_t stream) {
+  moe_status st = check_desc(d);
+  if (st) return st;
+  if (d->n_shared > 0) NEED(x);
+  if (d->local_count > 0) { NEED(x_perm); NEED(offsets); }
+  NEED(w_gate); NEED(w_up); NEED(w_down); NEED(y_perm); NEED(saved);
+  NEED_WS(ws_bytes, ffn_fwd_ws_bytes(*d));
+  return hip_status(launch_ffn_fwd(*d, x, x_perm, offsets, w_gate, w_up, w_down, y_perm, saved, ws, stream),
+                    "moe_expert_ffn_fwd");
+}
+
+moe_status moe_combine(const moe_desc* d, const void* y_perm, const int32_t* slot_to_row, const float* topk_w,
+                       void* y, hipStream_t stream) {
+  moe_status st = check_desc(d);
+  if (st) return st;
+  NEED(y_perm); NEED(slot_to_row); NEED(topk_w); NEED(y);
+  return hip_status(launch_combine(*d, y_perm, slot_to_row, topk_w, y, stream), "moe_combine");
+}
+
+moe_status moe_combine_bwd(const moe_desc* d, const void* dy, const void* y_perm, const int32_t* slot_to_row,
+                           const float* topk_w, void* dy_perm, float* dgate, hipStream_t stream) {
+  moe_status st = check_desc(d);
+  if (st) return st;
+  NEED(dy); NEED(y_perm); NEED(slot_to_row); NEED(topk_w); NEED(dy_perm); NEED(dgate);
+  return hip_status(launch_combine_bwd(*d, dy, y_perm, slot_to_row, topk_w, dy_perm, dgate, stream),
+                    "moe_combine_bwd");
+}
+
+moe_status moe_expert_ffn_bwd(const moe_desc* d, const void* x, const void* x_perm, const void* dy,
+                              const void* dy_perm, const int32_t* offsets, const void* w_gate, const void* w_up,
+                              const void* w_down, const void* saved, void* dx_perm, void* dw_gate, void* dw_up,
+                              void* dw_down, void* ws, size_t ws_bytes, hipStream_t stream) {
+  moe_status st = check_desc(d);
+  if (st) return st;
+  if (d->n_shared > 0) { NEED(x); NEED(dy); }
+  if (d->local_count > 0) { NEED(x_perm); NEED(dy_perm); NEED(offsets); }
+  NEED(w_gate); NEED(w_up); NEED(w_down); NEED(saved); NEED(dx_perm); NEED(dw_gate); NEED(dw_up); NEED(dw_down);
+  NEED_WS(ws_bytes, ffn_bwd_ws_bytes(*d));
+  return hip_status(launch_ffn_bwd(*d, x, x_perm, dy, dy_perm, offsets, w_gate, w_up, w_down, saved, dx_perm,
+                                   dw_gate, dw_up, dw_down, ws, stream),
+                    "moe_expert_ffn_bwd");
+}
+
+moe_status moe_route_bwd(const moe_desc* d, const void* x, const float* logits, const int32_t* topk_idx,
+                         const float* topk_w, const float* dgate, float* dlogits, float* dw_router, void* ws,
+                         size_t ws_bytes, hipStream_t stream) {
+  moe_status st = check_desc(d);
+  if (st) return st;
+  if (d->local_begin != 0 || d->local_count != d->n_experts)
+    return fail(MOE_ERR_INVALID_ARGUMENT,
+                "moe_route_bwd needs every expert's dgate (local range must be [0, E)); a party shard leaves the "
+                "router gradient to the data owner");
+  NEED(x); NEED(topk_idx); NEED(topk_w); NEED(dgate); NEED(dlogits); NEED(dw_router);
+  if (!d->renormalize) NEED(logits);
+  NEED_WS(ws_bytes, route_bwd_ws_bytes(*d));
+  return hip_status(launch_route_bwd(*d, x, logits, topk_idx, topk_w, dgate, dlogits, dw_router, ws, stream),
+                    "moe_route_bwd");
+}
+
+moe_status moe_permute_bwd(const moe_desc* d, const void* dx_perm, const int32_t* slot_to_row, const float* dlogits,
+                           const void* w_router, void* dx, hipStream_t stream) {
+  moe_status st = check_desc(d);
+  if (st) return st;
+  NEED(dx_perm); NEED(slot_to_row); NEED(dx);
+  if (dlogits) NEED(w_router);
+  return hip_status(launch_permute_bwd(*d, dx_perm, slot_to_row, dlogits, w_router, dx, stream), "moe_permute_bwd");
+}
+
+moe_status moe_kernel_timing(int enable) {
+  TimingState& ts = timing();
+  std::lock_guard<std::mutex> lk(ts.mu);
+  for (auto& r : ts.recs) {
+    ts.pool.push_back(r.a);
+    ts.pool.push_back(r.b);
+  }
+  ts.recs.clear();
+  ts.on = enable != 0;
+  return MOE_OK;
+}
+
+size_t moe_kernel_timing_report(char* buf, size_t n) {
+  TimingState& ts = timing();
+  std::lock_guard<std::mutex> lk(ts.mu);
+  std::map<std::string, std::pair<long, double>> agg;
+  std::vector<std::string> order;
+  for (auto& r : ts.recs) {
+    float ms = 0.f;
+    if (hipEventSynchronize(r.b) != hipSuccess || hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) continue;
+    auto it = agg.find(r.name);
+    if (it == agg.end()) {
+      order.push_back(r.name);
+      agg[r.name] = {1, (double)ms};
+    } else {
+      it->second.first += 1;
+      it->second.second += ms;
+    }
+  }
+  std::string out;
+  for (auto& nm : order) {
+    char line[256];
+    snprintf(line, sizeof(line), "%s %ld %.6f\n", nm.c_str(), agg[nm].first, agg[nm].second);
+    out += line;
+  }
+  if (buf && n) {
+    size_t m = out.size() < n - 1 ? out.size() : n - 1;
+    memcpy(buf, out.data(), m);
+    buf[m] = 0;
+  }
+  return out.size() + 1;
+}
+
+}  // extern "C"

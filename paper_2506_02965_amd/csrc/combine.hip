@@ -1,0 +1,124 @@
+// Owner-side combine of Alg. 3 (y_t = sum over the token's selected experts of w * output, plus
+// the always-active shared experts) and its adjoint (Alg. 5 / Sec. 3.2: each host receives the
+// gradient w.r.t. its expert's output, w * dY; the owner keeps dgate = <dY, output>).
+// One wavefront per token; 16-byte chunks along d; fp32 sums in slot order, then shared experts.
+#include "pcmoe_internal.h"
+
+namespace pcmoe {
+
+static int token_blocks(int Tn) {
+  int b = (Tn + 3) / 4;
+  return b > 8192 ? 8192 : (b < 1 ? 1 : b);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void combine_kernel(int Tn, int k, int S, int cpr, const Chunk* __restrict__ yp,
+                                                      const int32_t* __restrict__ s2r,
+                                                      const float* __restrict__ gw, Chunk* __restrict__ y) {
+  constexpr int N = EPC<T>::value;
+  const int lane = threadIdx.x & 63;
+  const int wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int nwaves = (gridDim.x * blockDim.x) >> 6;
+  const size_t shared_base = (size_t)Tn * k;
+  for (int t = wave; t < Tn; t += nwaves) {
+    int rows[8];
+    float w[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      rows[j] = (j < k) ? s2r[(size_t)t * k + j] : -1;
+      w[j] = (j < k) ? gw[(size_t)t * k + j] : 0.f;
+    }
+    for (int c = lane; c < cpr; c += 64) {
+      float acc[N], v[N];
+#pragma unroll
+      for (int i = 0; i < N; ++i) acc[i] = 0.f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (rows[j] >= 0) {
+          chunk_to_f<T>(yp[(size_t)rows[j] * cpr + c], v);
+#pragma unroll
+          for (int i = 0; i < N; ++i) acc[i] = fmaf(w[j], v[i], acc[i]);
+        }
+      }
+      for (int sh = 0; sh < S; ++sh) {
+        chunk_to_f<T>(yp[(shared_base + (size_t)sh * Tn + t) * cpr + c], v);
+#pragma unroll
+        for (int i = 0; i < N; ++i) acc[i] += v[i];
+      }
+      y[(size_t)t * cpr + c] = f_to_chunk<T>(acc);
+    }
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void combine_bwd_kernel(int Tn, int k, int cpr, const Chunk* __restrict__ dy,
+                                                          const Chunk* __restrict__ yp,
+                                                          const int32_t* __restrict__ s2r,
+                                                          const float* __restrict__ gw, Chunk* __restrict__ dyp,
+                                                          float* __restrict__ dgate) {
+  constexpr int N = EPC<T>::value;
+  const int lane = threadIdx.x & 63;
+  const int wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int nwaves = (gridDim.x * blockDim.x) >> 6;
+  for (int t = wave; t < Tn; t += nwaves) {
+    int rows[8];
+    float w[8], dot[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      rows[j] = (j < k) ? s2r[(size_t)t * k + j] : -1;
+      w[j] = (j < k) ? gw[(size_t)t * k + j] : 0.f;
+      dot[j] = 0.f;
+    }
+    for (int c = lane; c < cpr; c += 64) {
+      float g[N], o[N], s[N];
+      chunk_to_f<T>(dy[(size_t)t * cpr + c], g);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (rows[j] >= 0) {
+          chunk_to_f<T>(yp[(size_t)rows[j] * cpr + c], o);
+#pragma unroll
+          for (int i = 0; i < N; ++i) {
+            dot[j] = fmaf(g[i], o[i], dot[j]);
+            s[i] = w[j] * g[i];
+          }
+          dyp[(size_t)rows[j] * cpr + c] = f_to_chunk<T>(s);
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (j < k) {
+        float tot = wave_sum(dot[j]);
+        if (lane == 0) dgate[(size_t)t * k + j] = (rows[j] >= 0) ? tot : 0.f;
+      }
+    }
+  }
+}
+
+hipError_t launch_combine(const moe_desc& d, const void* yp, const int32_t* s2r, const float* w, void* y,
+                          hipStream_t s) {
+  const int cpr = (int)(d.d_model * elem_bytes(d) / 16);
+  KernelTimer kt("combine", s);
+  if (d.dtype == MOE_BF16)
+    hipLaunchKernelGGL(combine_kernel<bf16>, dim3(token_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k, d.n_shared,
+                       cpr, (const Chunk*)yp, s2r, w, (Chunk*)y);
+  else
+    hipLaunchKernelGGL(combine_kernel<float>, dim3(token_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k, d.n_shared,
+                       cpr, (const Chunk*)yp, s2r, w, (Chunk*)y);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine_bwd(const moe_desc& d, const void* dy, const void* yp, const int32_t* s2r,
+                              const float* w, void* dyp, float* dgate, hipStream_t s) {
+  const int cpr = (int)(d.d_model * elem_bytes(d) / 16);
+  KernelTimer kt("combine_bwd", s);
+  if (d.dtype == MOE_BF16)
+    hipLaunchKernelGGL(combine_bwd_kernel<bf16>, dim3(token_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k, cpr,
+                       (const Chunk*)dy, (const Chunk*)yp, s2r, w, (Chunk*)dyp, dgate);
+  else
+    hipLaunchKernelGGL(combine_bwd_kernel<float>, dim3(token_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k, cpr,
+                       (const Chunk*)dy, (const Chunk*)yp, s2r, w, (Chunk*)dyp, dgate);
+  return hipGetLastError();
+}
+
+}  // namespace pcmoe

@@ -1,0 +1,135 @@
+// Private helpers of the pcmoe HIP library (gfx950 / CDNA4). Not part of the ABI.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include "../../include/pcmoe.h"
+
+namespace pcmoe {
+
+typedef uint16_t bf16;  // bfloat16 storage (upper half of an IEEE binary32)
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// 16-byte chunk: the unit of every global and LDS transfer of the hot kernels.
+struct __align__(16) Chunk {
+  uint32_t w[4];
+};
+
+__device__ __forceinline__ float bf2f(bf16 v) { return __uint_as_float(((uint32_t)v) << 16); }
+
+// float -> bfloat16, round to nearest, ties to even (finite values).
+__device__ __forceinline__ bf16 f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16)(u >> 16);
+}
+
+__device__ __forceinline__ float to_f(float v) { return v; }
+__device__ __forceinline__ float to_f(bf16 v) { return bf2f(v); }
+template <typename T> __device__ __forceinline__ T from_f(float v);
+template <> __device__ __forceinline__ float from_f<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16 from_f<bf16>(float v) { return f2bf(v); }
+
+// Elements of type T in one 16-byte chunk.
+template <typename T> struct EPC;
+template <> struct EPC<float> { static constexpr int value = 4; };
+template <> struct EPC<bf16> { static constexpr int value = 8; };
+
+// Unpack / pack a chunk to / from fp32 values.
+template <typename T> __device__ __forceinline__ void chunk_to_f(const Chunk& c, float* out);
+template <> __device__ __forceinline__ void chunk_to_f<float>(const Chunk& c, float* out) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) out[i] = __uint_as_float(c.w[i]);
+}
+template <> __device__ __forceinline__ void chunk_to_f<bf16>(const Chunk& c, float* out) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    out[2 * i] = __uint_as_float(c.w[i] << 16);
+    out[2 * i + 1] = __uint_as_float(c.w[i] & 0xffff0000u);
+  }
+}
+template <typename T> __device__ __forceinline__ Chunk f_to_chunk(const float* in);
+template <> __device__ __forceinline__ Chunk f_to_chunk<float>(const float* in) {
+  Chunk c;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) c.w[i] = __float_as_uint(in[i]);
+  return c;
+}
+template <> __device__ __forceinline__ Chunk f_to_chunk<bf16>(const float* in) {
+  Chunk c;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) c.w[i] = (uint32_t)f2bf(in[2 * i]) | ((uint32_t)f2bf(in[2 * i + 1]) << 16);
+  return c;
+}
+
+__device__ __forceinline__ Chunk ld_chunk(const void* p) { return *reinterpret_cast<const Chunk*>(p); }
+__device__ __forceinline__ void st_chunk(void* p, const Chunk& c) { *reinterpret_cast<Chunk*>(p) = c; }
+__device__ __forceinline__ Chunk zero_chunk() {
+  Chunk c;
+  c.w[0] = c.w[1] = c.w[2] = c.w[3] = 0u;
+  return c;
+}
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+  return v;
+}
+
+// ---------------------------------------------------------------- host side
+
+// Bracket a kernel launch with HIP events when per-kernel timing is on (no-op otherwise).
+struct KernelTimer {
+  KernelTimer(const char* name, hipStream_t s);
+  ~KernelTimer();
+  const char* name;
+  hipStream_t stream;
+  void* slot;
+};
+
+// Launchers (defined next to their kernels). All return hipSuccess or the launch error.
+hipError_t launch_route_fwd(const moe_desc& d, const void* x, const void* wr, const float* bias, int bias_groups,
+                            float* logits, int32_t* idx, float* w, hipStream_t s);
+hipError_t launch_route_bwd(const moe_desc& d, const void* x, const float* logits, const int32_t* idx,
+                            const float* w, const float* dgate, float* dlogits, float* dwr, void* ws,
+                            hipStream_t s);
+size_t route_bwd_ws_bytes(const moe_desc& d);
+
+hipError_t launch_permute(const moe_desc& d, const int32_t* idx, const void* x, int32_t* counts, int32_t* offsets,
+                          int32_t* r2s, int32_t* s2r, void* xp, void* ws, hipStream_t s);
+size_t permute_ws_bytes(const moe_desc& d);
+hipError_t launch_permute_bwd(const moe_desc& d, const void* dxp, const int32_t* s2r, const float* dlogits,
+                              const void* wr, void* dx, hipStream_t s);
+
+hipError_t launch_combine(const moe_desc& d, const void* yp, const int32_t* s2r, const float* w, void* y,
+                          hipStream_t s);
+hipError_t launch_combine_bwd(const moe_desc& d, const void* dy, const void* yp, const int32_t* s2r,
+                              const float* w, void* dyp, float* dgate, hipStream_t s);
+
+size_t ffn_saved_bytes(const moe_desc& d);
+size_t ffn_fwd_ws_bytes(const moe_desc& d);
+size_t ffn_bwd_ws_bytes(const moe_desc& d);
+hipError_t launch_ffn_fwd(const moe_desc& d, const void* x, const void* xp, const int32_t* offsets,
+                          const void* wg, const void* wu, const void* wd, void* yp, void* saved, void* ws,
+                          hipStream_t s);
+hipError_t launch_ffn_bwd(const moe_desc& d, const void* x, const void* xp, const void* dy, const void* dyp,
+                          const int32_t* offsets, const void* wg, const void* wu, const void* wd,
+                          const void* saved, void* dxp, void* dwg, void* dwu, void* dwd, void* ws,
+                          hipStream_t s);
+
+inline size_t elem_bytes(const moe_desc& d) { return d.dtype == MOE_BF16 ? 2 : 4; }
+inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+inline int64_t rows_total(const moe_desc& d) {
+  return (int64_t)d.T * d.top_k + (int64_t)d.n_shared * d.T;
+}
+
+}  // namespace pcmoe

@@ -1,0 +1,268 @@
+// Dispatch of Alg. 3 ("Send h to the host of each selected expert") as a stable counting sort
+// of the hosted assignment slots a = t*k + j by expert, plus the gather of their token rows;
+// and the hand-back of the input gradient (Sec. 3.2), summed per token.
+//
+// Ordering is reproducible bit for bit: rows of one expert are in increasing slot order.
+//   1. histogram: per block of PM_SLOTS slots, per hosted expert counts (LDS atomics; order-free)
+//   2. scan: per expert, exclusive prefix over blocks, then over experts -> offsets
+//   3. scatter: inside a block, each wavefront ranks its 64 slots with ballots (lanes holding
+//      the same expert form a peer mask; rank = popcount of lower peers), waves in order.
+//   4. gather: one wavefront per token reads its row once and writes its k destinations.
+#include "pcmoe_internal.h"
+
+namespace pcmoe {
+
+constexpr int PM_SLOTS = 1024;  // slots per block (4 waves x 4 x 64)
+
+__device__ __forceinline__ uint64_t peer_mask(int v, bool valid, int nbits) {
+  uint64_t peers = __ballot(valid);
+  for (int b = 0; b < nbits; ++b) {
+    const bool bit = (v >> b) & 1;
+    const uint64_t m = __ballot(bit);
+    peers &= bit ? m : ~m;
+  }
+  return peers;
+}
+
+__global__ __launch_bounds__(256) void perm_hist_kernel(const int32_t* __restrict__ idx, int nslots, int lb,
+                                                        int lc, int32_t* __restrict__ blk_counts) {
+  extern __shared__ int hist[];
+  for (int e = threadIdx.x; e < lc; e += 256) hist[e] = 0;
+  __syncthreads();
+  const int a0 = blockIdx.x * PM_SLOTS;
+  for (int i = threadIdx.x; i < PM_SLOTS; i += 256) {
+    int a = a0 + i;
+    if (a < nslots) {
+      int v = idx[a] - lb;
+      if (v >= 0 && v < lc) atomicAdd(&hist[v], 1);
+    }
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < lc; e += 256) blk_counts[(size_t)blockIdx.x * lc + e] = hist[e];
+}
+
+// One block: per-expert totals, offsets and per-(block, expert) bases.
+__global__ __launch_bounds__(256) void perm_scan_kernel(int nblk, int lc, const int32_t* __restrict__ blk_counts,
+                                                        int32_t* __restrict__ blk_base, int32_t* __restrict__ counts,
+                                                        int32_t* __restrict__ offsets) {
+  __shared__ int tot[256];
+  __shared__ int wsum[4];
+  const int e = threadIdx.x;
+  int run = 0;
+  if (e < lc)
+    for (int b = 0; b < nblk; ++b) run += blk_counts[(size_t)b * lc + e];
+  tot[e] = (e < lc) ? run : 0;
+  __syncthreads();
+  // exclusive scan of tot[0..255] (lc <= 256)
+  const int lane = e & 63, w = e >> 6;
+  int v = tot[e];
+  int incl = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    int o = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += o;
+  }
+  if (lane == 63) wsum[w] = incl;
+  __syncthreads();
+  int base = 0;
+  for (int i = 0; i < w; ++i) base += wsum[i];
+  const int excl = base + incl - v;
+  if (e < lc) {
+    counts[e] = v;
+    offsets[e] = excl;
+    int r = excl;
+    for (int b = 0; b < nblk; ++b) {
+      blk_base[(size_t)b * lc + e] = r;
+      r += blk_counts[(size_t)b * lc + e];
+    }
+  }
+  if (e == lc - 1) offsets[lc] = excl + v;
+}
+
+__global__ __launch_bounds__(256) void perm_scatter_kernel(const int32_t* __restrict__ idx, int nslots, int lb,
+                                                           int lc, int nbits,
+                                                           const int32_t* __restrict__ blk_base,
+                                                           const int32_t* __restrict__ offsets,
+                                                           int32_t* __restrict__ r2s, int32_t* __restrict__ s2r) {
+  extern __shared__ int wcnt[];  // [4][lc]
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  for (int i = threadIdx.x; i < 4 * lc; i += 256) wcnt[i] = 0;
+  __syncthreads();
+  const int a_w = blockIdx.x * PM_SLOTS + w * (PM_SLOTS / 4);
+  const uint64_t lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
+  int* mine = wcnt + w * lc;
+  // pass 1: per-wave counts
+  for (int it = 0; it < PM_SLOTS / 4 / 64; ++it) {
+    const int a = a_w + it * 64 + lane;
+    int v = (a < nslots) ? idx[a] - lb : -1;
+    const bool loc = (v >= 0 && v < lc);
+    if (!loc) v = 0;
+    const uint64_t peers = peer_mask(v, loc, nbits);
+    if (loc && (peers & lt) == 0) mine[v] += __popcll(peers);
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < lc; e += 256) {
+    int r = blk_base[(size_t)blockIdx.x * lc + e];
+    for (int ww = 0; ww < 4; ++ww) {
+      int c = wcnt[ww * lc + e];
+      wcnt[ww * lc + e] = r;
+      r += c;
+    }
+  }
+  __syncthreads();
+  // pass 2: stable ranks
+  for (int it = 0; it < PM_SLOTS / 4 / 64; ++it) {
+    const int a = a_w + it * 64 + lane;
+    int v = (a < nslots) ? idx[a] - lb : -1;
+    const bool loc = (v >= 0 && v < lc);
+    if (!loc) v = 0;
+    const uint64_t peers = peer_mask(v, loc, nbits);
+    int pos = 0;
+    if (loc) pos = mine[v] + __popcll(peers & lt);
+    if (a < nslots) {
+      if (loc) {
+        r2s[pos] = a;
+        s2r[a] = pos;
+      } else {
+        s2r[a] = -1;
+      }
+    }
+    if (loc && (peers & lt) == 0) mine[v] += __popcll(peers);
+  }
+  // rows beyond N_loc have no slot
+  const int nloc = offsets[lc];
+  for (int i = threadIdx.x; i < PM_SLOTS; i += 256) {
+    int r = blockIdx.x * PM_SLOTS + i;
+    if (r < nslots && r >= nloc) r2s[r] = -1;
+  }
+}
+
+// Token-major gather: x_perm[slot_to_row[t*k+j]] = x[t] for every hosted slot.
+__global__ __launch_bounds__(256) void perm_gather_kernel(int Tn, int k, int cpr, const Chunk* __restrict__ x,
+                                                          const int32_t* __restrict__ s2r, Chunk* __restrict__ xp) {
+  const int lane = threadIdx.x & 63;
+  const int wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int nwaves = (gridDim.x * blockDim.x) >> 6;
+  for (int t = wave; t < Tn; t += nwaves) {
+    int rows[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) rows[j] = (j < k) ? s2r[(size_t)t * k + j] : -1;
+    for (int c = lane; c < cpr; c += 64) {
+      const Chunk v = x[(size_t)t * cpr + c];
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (rows[j] >= 0) xp[(size_t)rows[j] * cpr + c] = v;
+    }
+  }
+}
+
+static int nbits_for(int lc) {
+  int nb = 0;
+  while ((1 << nb) < lc) ++nb;
+  return nb;
+}
+
+size_t permute_ws_bytes(const moe_desc& d) {
+  size_t nslots = (size_t)d.T * d.top_k;
+  size_t nblk = (nslots + PM_SLOTS - 1) / PM_SLOTS;
+  return 2 * align256(nblk * d.local_count * sizeof(int32_t));
+}
+
+static int gather_blocks(int Tn) {
+  int b = (Tn + 3) / 4;
+  return b > 8192 ? 8192 : (b < 1 ? 1 : b);
+}
+
+hipError_t launch_permute(const moe_desc& d, const int32_t* idx, const void* x, int32_t* counts, int32_t* offsets,
+                          int32_t* r2s, int32_t* s2r, void* xp, void* ws, hipStream_t s) {
+  const int nslots = d.T * d.top_k;
+  const int nblk = (nslots + PM_SLOTS - 1) / PM_SLOTS;
+  const int lc = d.local_count;
+  int32_t* blk_counts = (int32_t*)ws;
+  int32_t* blk_base = (int32_t*)((char*)ws + align256((size_t)nblk * lc * sizeof(int32_t)));
+  {
+    KernelTimer kt("permute_hist", s);
+    hipLaunchKernelGGL(perm_hist_kernel, dim3(nblk), dim3(256), lc * sizeof(int), s, idx, nslots, d.local_begin, lc,
+                       blk_counts);
+  }
+  {
+    KernelTimer kt("permute_scan", s);
+    hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(256), 0, s, nblk, lc, blk_counts, blk_base, counts, offsets);
+  }
+  {
+    KernelTimer kt("permute_scatter", s);
+    hipLaunchKernelGGL(perm_scatter_kernel, dim3(nblk), dim3(256), 4 * lc * sizeof(int), s, idx, nslots,
+                       d.local_begin, lc, nbits_for(lc), blk_base, offsets, r2s, s2r);
+  }
+  {
+    KernelTimer kt("permute_gather", s);
+    const int cpr = (int)(d.d_model * elem_bytes(d) / 16);
+    hipLaunchKernelGGL(perm_gather_kernel, dim3(gather_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k, cpr,
+                       (const Chunk*)x, s2r, (Chunk*)xp);
+  }
+  return hipGetLastError();
+}
+
+// dx_t = sum_j dx_perm[row(t,j)] + sum_s dx_perm[T*k + s*T + t] (+ sum_e dlogits[t,e] * w_router[e])
+template <typename T>
+__global__ __launch_bounds__(256) void unpermute_kernel(int Tn, int k, int S, int E, int cpr,
+                                                        const Chunk* __restrict__ dxp,
+                                                        const int32_t* __restrict__ s2r,
+                                                        const float* __restrict__ dl,
+                                                        const Chunk* __restrict__ wr, Chunk* __restrict__ dx) {
+  constexpr int N = EPC<T>::value;
+  const int lane = threadIdx.x & 63;
+  const int wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int nwaves = (gridDim.x * blockDim.x) >> 6;
+  const size_t shared_base = (size_t)Tn * k;
+  for (int t = wave; t < Tn; t += nwaves) {
+    int rows[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) rows[j] = (j < k) ? s2r[(size_t)t * k + j] : -1;
+    for (int c = lane; c < cpr; c += 64) {
+      float acc[N];
+#pragma unroll
+      for (int i = 0; i < N; ++i) acc[i] = 0.f;
+      float v[N];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (rows[j] >= 0) {
+          chunk_to_f<T>(dxp[(size_t)rows[j] * cpr + c], v);
+#pragma unroll
+          for (int i = 0; i < N; ++i) acc[i] += v[i];
+        }
+      }
+      for (int sh = 0; sh < S; ++sh) {
+        chunk_to_f<T>(dxp[(shared_base + (size_t)sh * Tn + t) * cpr + c], v);
+#pragma unroll
+        for (int i = 0; i < N; ++i) acc[i] += v[i];
+      }
+      if (dl) {
+        for (int e = 0; e < E; ++e) {
+          const float g = dl[(size_t)t * E + e];
+          if (g != 0.f) {
+            chunk_to_f<T>(wr[(size_t)e * cpr + c], v);
+#pragma unroll
+            for (int i = 0; i < N; ++i) acc[i] = fmaf(g, v[i], acc[i]);
+          }
+        }
+      }
+      dx[(size_t)t * cpr + c] = f_to_chunk<T>(acc);
+    }
+  }
+}
+
+hipError_t launch_permute_bwd(const moe_desc& d, const void* dxp, const int32_t* s2r, const float* dl,
+                              const void* wr, void* dx, hipStream_t s) {
+  const int cpr = (int)(d.d_model * elem_bytes(d) / 16);
+  KernelTimer kt("unpermute", s);
+  if (d.dtype == MOE_BF16)
+    hipLaunchKernelGGL(unpermute_kernel<bf16>, dim3(gather_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k, d.n_shared,
+                       d.n_experts, cpr, (const Chunk*)dxp, s2r, dl, (const Chunk*)wr, (Chunk*)dx);
+  else
+    hipLaunchKernelGGL(unpermute_kernel<float>, dim3(gather_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k,
+                       d.n_shared, d.n_experts, cpr, (const Chunk*)dxp, s2r, dl, (const Chunk*)wr, (Chunk*)dx);
+  return hipGetLastError();
+}
+
+}  // namespace pcmoe

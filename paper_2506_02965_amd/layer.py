@@ -1,0 +1,138 @@
+"""One MoE expert layer on the GPU: torch owns the buffers, libpcmoe computes every step.
+
+Forward (Alg. 3 with the gating of Alg. 7 and the experts of Alg. 6):
+    moe_route -> moe_permute -> moe_expert_ffn_fwd -> moe_combine
+Backward (Alg. 5 / Alg. 6 and the owner-side router adjoint):
+    moe_combine_bwd -> moe_expert_ffn_bwd -> moe_route_bwd (full layer only) -> moe_permute_bwd
+All calls are enqueued on one stream; no per-expert count ever returns to the host.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+import torch
+
+from . import pcmoe as P
+
+
+@dataclass
+class LayerWeights:
+    x: torch.Tensor
+    w_router: torch.Tensor
+    logit_bias: Optional[torch.Tensor]
+    bias_groups: int
+    w_gate: torch.Tensor
+    w_up: torch.Tensor
+    w_down: torch.Tensor
+    dy: Optional[torch.Tensor] = None
+
+
+def torch_dtype(dtype: str):
+    return torch.bfloat16 if dtype == "bf16" else torch.float32
+
+
+def upload(inp, device="cuda") -> LayerWeights:
+    """Copy a synth.LayerInputs (float32 arrays, bf16-exact for bf16 layers) to the device."""
+    cfg = inp.cfg
+    dt = torch_dtype(cfg.dtype)
+    to = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device=device).to(dt)
+    bias = None
+    if inp.logit_bias is not None:
+        bias = torch.from_numpy(np.ascontiguousarray(inp.logit_bias, dtype=np.float32)).to(device)
+    return LayerWeights(to(inp.x), to(inp.w_router), bias, cfg.bias_groups, to(inp.w_gate), to(inp.w_up),
+                        to(inp.w_down), None if inp.dy is None else to(inp.dy))
+
+
+class MoELayer:
+    def __init__(self, cfg, device="cuda", backward=None, router_backward=None):
+        self.cfg = cfg
+        self.device = device
+        self.backward_enabled = cfg.backward if backward is None else backward
+        self.router_backward = cfg.router_backward if router_backward is None else router_backward
+        self.desc = P.make_desc(cfg.T, cfg.d, cfg.f, cfg.E, cfg.k, cfg.local_begin, cfg.n_local, cfg.n_shared,
+                                cfg.renormalize, cfg.dtype)
+        T, d, f, E, k, S, Eloc = cfg.T, cfg.d, cfg.f, cfg.E, cfg.k, cfg.n_shared, cfg.n_local
+        dt = torch_dtype(cfg.dtype)
+        R = T * k + S * T
+        kw = dict(device=device)
+        self.logits = torch.empty(T, E, dtype=torch.float32, **kw)
+        self.topk_idx = torch.empty(T, k, dtype=torch.int32, **kw)
+        self.topk_w = torch.empty(T, k, dtype=torch.float32, **kw)
+        self.counts = torch.empty(max(Eloc, 1), dtype=torch.int32, **kw)
+        self.offsets = torch.empty(Eloc + 1, dtype=torch.int32, **kw)
+        self.row_to_slot = torch.empty(T * k, dtype=torch.int32, **kw)
+        self.slot_to_row = torch.empty(T * k, dtype=torch.int32, **kw)
+        self.x_perm = torch.empty(T * k, d, dtype=dt, **kw)
+        self.y_perm = torch.empty(R, d, dtype=dt, **kw)
+        self.y = torch.empty(T, d, dtype=dt, **kw)
+        ws = lambda which: torch.empty(max(P.moe_workspace_size(self.desc, which), 1), dtype=torch.uint8, **kw)
+        self.ws_permute = ws(P.MOE_WS_PERMUTE)
+        self.saved = ws(P.MOE_WS_FFN_SAVED)
+        self.ws_ffn_fwd = ws(P.MOE_WS_FFN_FWD)
+        if self.backward_enabled:
+            G = Eloc + S
+            self.dy_perm = torch.empty(T * k, d, dtype=dt, **kw)
+            self.dgate = torch.empty(T, k, dtype=torch.float32, **kw)
+            self.dx_perm = torch.empty(R, d, dtype=dt, **kw)
+            self.dw_gate = torch.empty(G, f, d, dtype=dt, **kw)
+            self.dw_up = torch.empty(G, f, d, dtype=dt, **kw)
+            self.dw_down = torch.empty(G, d, f, dtype=dt, **kw)
+            self.ws_ffn_bwd = ws(P.MOE_WS_FFN_BWD)
+            self.dx = torch.empty(T, d, dtype=dt, **kw)
+            if self.router_backward:
+                self.dlogits = torch.empty(T, E, dtype=torch.float32, **kw)
+                self.dw_router = torch.empty(E, d, dtype=torch.float32, **kw)
+                self.ws_route_bwd = ws(P.MOE_WS_ROUTE_BWD)
+
+    # ------------------------------------------------------------------ forward
+    def route(self, w: LayerWeights):
+        P.moe_route(self.desc, w.x, w.w_router, w.logit_bias, w.bias_groups, self.logits, self.topk_idx, self.topk_w)
+
+    def permute(self, w: LayerWeights):
+        P.moe_permute(self.desc, self.topk_idx, w.x, self.counts, self.offsets, self.row_to_slot, self.slot_to_row,
+                      self.x_perm, self.ws_permute, self.ws_permute.numel())
+
+    def ffn_fwd(self, w: LayerWeights):
+        P.moe_expert_ffn_fwd(self.desc, w.x, self.x_perm, self.offsets, w.w_gate, w.w_up, w.w_down, self.y_perm,
+                             self.saved, self.ws_ffn_fwd, self.ws_ffn_fwd.numel())
+
+    def combine(self):
+        P.moe_combine(self.desc, self.y_perm, self.slot_to_row, self.topk_w, self.y)
+
+    def forward(self, w: LayerWeights):
+        self.route(w)
+        self.permute(w)
+        self.ffn_fwd(w)
+        self.combine()
+        return self.y
+
+    # ----------------------------------------------------------------- backward
+    def combine_bwd(self, dy):
+        P.moe_combine_bwd(self.desc, dy, self.y_perm, self.slot_to_row, self.topk_w, self.dy_perm, self.dgate)
+
+    def ffn_bwd(self, w: LayerWeights, dy):
+        P.moe_expert_ffn_bwd(self.desc, w.x, self.x_perm, dy, self.dy_perm, self.offsets, w.w_gate, w.w_up, w.w_down,
+                             self.saved, self.dx_perm, self.dw_gate, self.dw_up, self.dw_down, self.ws_ffn_bwd,
+                             self.ws_ffn_bwd.numel())
+
+    def route_bwd(self, w: LayerWeights):
+        P.moe_route_bwd(self.desc, w.x, self.logits, self.topk_idx, self.topk_w, self.dgate, self.dlogits,
+                        self.dw_router, self.ws_route_bwd, self.ws_route_bwd.numel())
+
+    def permute_bwd(self, w: LayerWeights):
+        P.moe_permute_bwd(self.desc, self.dx_perm, self.slot_to_row, self.dlogits if self.router_backward else None,
+                          w.w_router, self.dx)
+
+    def backward(self, w: LayerWeights, dy=None):
+        dy = w.dy if dy is None else dy
+        self.combine_bwd(dy)
+        self.ffn_bwd(w, dy)
+        if self.router_backward:
+            self.route_bwd(w)
+        self.permute_bwd(w)
+        return self.dx
+
+    def n_local_rows(self) -> int:
+        return int(self.offsets[-1].item())

@@ -16,13 +16,15 @@ are not published; Sec. 4 setup, Table 1):
         logit bias log p_e with p ~ Zipf(s=1.1) over experts
 
 Draw recipe: every tensor has its own numpy PCG64 stream keyed by (seed, tag, expert), drawn
-as float64 standard normals, scaled, cast to float32, and for bf16 workloads rounded once to
+as float32 standard normals, scaled in float32, and for bf16 workloads rounded once to
 bf16 (round-to-nearest-even). x ~ N(0,1); dY ~ N(0,1); router and gate/up weights
 ~ N(0, 1/d); down weights ~ N(0, 1/f) (variance 1/fan_in).
 """
 from __future__ import annotations
 
 import dataclasses
+import os
+from concurrent.futures import ThreadPoolExecutor
 from typing import Optional
 
 import numpy as np
@@ -83,16 +85,19 @@ CONFIGS = {
 def round_to_bf16(a: np.ndarray) -> np.ndarray:
     """Round float32 values to the nearest bfloat16 (ties to even); returns float32 holding them.
 
-    Finite inputs only (the draws are Gaussian)."""
-    a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
-    return u.astype(np.uint32).view(np.float32)
+    Finite inputs only (the draws are Gaussian), so the uint32 sum cannot wrap."""
+    u = np.array(a, dtype=np.float32, copy=True, order="C").view(np.uint32)
+    u += np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))
+    u &= np.uint32(0xFFFF0000)
+    return u.view(np.float32)
 
 
 def _normal(seed: int, tag: int, idx: int, shape, std: float) -> np.ndarray:
     rng = np.random.default_rng([seed, tag, idx])
-    return (rng.standard_normal(shape) * std).astype(np.float32)
+    a = rng.standard_normal(shape, dtype=np.float32)
+    if std != 1.0:
+        a *= np.float32(std)
+    return a
 
 
 def _store(a: np.ndarray, dtype: str) -> np.ndarray:
@@ -140,14 +145,24 @@ def make_inputs(cfg: LayerConfig, with_dy: Optional[bool] = None) -> LayerInputs
     w_gate = np.empty((G, f, d), np.float32)
     w_up = np.empty((G, f, d), np.float32)
     w_down = np.empty((G, d, f), np.float32)
-    for g in range(G):
+
+    def fill(job):
+        g, which = job
         if g < cfg.n_local:
-            eid, tg, tu, tdn = cfg.local_begin + g, TAG_GATE, TAG_UP, TAG_DOWN
+            eid, tags = cfg.local_begin + g, (TAG_GATE, TAG_UP, TAG_DOWN)
         else:
-            eid, tg, tu, tdn = g - cfg.n_local, TAG_SH_GATE, TAG_SH_UP, TAG_SH_DOWN
-        w_gate[g] = _store(_normal(s, tg, eid, (f, d), d ** -0.5), dt)
-        w_up[g] = _store(_normal(s, tu, eid, (f, d), d ** -0.5), dt)
-        w_down[g] = _store(_normal(s, tdn, eid, (d, f), f ** -0.5), dt)
+            eid, tags = g - cfg.n_local, (TAG_SH_GATE, TAG_SH_UP, TAG_SH_DOWN)
+        if which == 0:
+            w_gate[g] = _store(_normal(s, tags[0], eid, (f, d), d ** -0.5), dt)
+        elif which == 1:
+            w_up[g] = _store(_normal(s, tags[1], eid, (f, d), d ** -0.5), dt)
+        else:
+            w_down[g] = _store(_normal(s, tags[2], eid, (d, f), f ** -0.5), dt)
+
+    jobs = [(g, w) for g in range(G) for w in range(3)]
+    workers = max(1, min(16, os.cpu_count() or 1, len(jobs)))
+    with ThreadPoolExecutor(max_workers=workers) as ex:   # numpy's generators release the GIL
+        list(ex.map(fill, jobs))
     return LayerInputs(cfg, x, dy, w_router, bias, w_gate, w_up, w_down)
 
 

@@ -1,0 +1,98 @@
+"""Host-side checks of the C ABI: the library loads, exports every symbol include/pcmoe.h
+declares, sizes workspaces, and rejects bad arguments with the documented status before any
+HIP call (no GPU is touched here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2506_02965_amd import pcmoe as P
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+pytestmark = pytest.mark.skipif(not os.path.exists(P.LIB_PATH), reason="libpcmoe.so not built")
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "pcmoe.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(moe_\w+)\s*\(", src, flags=re.M)))
+
+
+def test_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) == 13, names
+    assert sorted(P.EXPORTS) == names
+    L = P.lib()
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def desc(**kw):
+    base = dict(T=256, d_model=256, d_ff=512, n_experts=8, top_k=2)
+    base.update(kw)
+    return P.make_desc(**base)
+
+
+def test_status_strings():
+    assert P.status_string(P.MOE_OK) == "MOE_OK"
+    assert P.status_string(P.MOE_ERR_WORKSPACE_TOO_SMALL) == "MOE_ERR_WORKSPACE_TOO_SMALL"
+
+
+def test_workspace_sizes():
+    d = desc(n_shared=1)
+    R = 256 * 2 + 256
+    assert P.moe_workspace_size(d, P.MOE_WS_FFN_SAVED) >= R * 3 * 512 * 2
+    assert P.moe_workspace_size(d, P.MOE_WS_FFN_BWD) >= R * 2 * 512 * 2
+    assert P.moe_workspace_size(d, P.MOE_WS_PERMUTE) > 0
+    assert P.moe_workspace_size(d, P.MOE_WS_ROUTE_BWD) >= 8 * 256 * 4
+    assert P.moe_workspace_size(desc(top_k=9), P.MOE_WS_PERMUTE) == 0   # invalid descriptor
+
+
+FAKE = 0x1000  # never dereferenced: every call below fails validation first
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(top_k=0), P.MOE_ERR_INVALID_ARGUMENT),
+    (dict(top_k=9, n_experts=16), P.MOE_ERR_UNSUPPORTED),
+    (dict(top_k=3, n_experts=2), P.MOE_ERR_INVALID_ARGUMENT),
+    (dict(local_begin=6, local_count=4), P.MOE_ERR_INVALID_ARGUMENT),
+    (dict(d_model=192), P.MOE_ERR_UNSUPPORTED),
+    (dict(d_ff=100), P.MOE_ERR_UNSUPPORTED),
+    (dict(n_experts=300), P.MOE_ERR_UNSUPPORTED),
+    (dict(dtype="bf16", renormalize=True, T=0), P.MOE_ERR_INVALID_ARGUMENT),
+])
+def test_descriptor_validation(kw, status):
+    d = desc(**kw)
+    with pytest.raises(P.MoeError) as ei:
+        P.moe_combine(d, FAKE, FAKE, FAKE, FAKE, stream=0)
+    assert ei.value.status == status
+
+
+def test_null_pointers_and_workspace():
+    d = desc()
+    with pytest.raises(P.MoeError) as ei:
+        P.moe_route(d, None, FAKE, None, 1, FAKE, FAKE, FAKE, stream=0)
+    assert ei.value.status == P.MOE_ERR_INVALID_ARGUMENT and "x" in P.last_error()
+    with pytest.raises(P.MoeError) as ei:
+        P.moe_route(d, FAKE, FAKE, FAKE, 3, FAKE, FAKE, FAKE, stream=0)   # 3 does not divide T=256
+    assert ei.value.status == P.MOE_ERR_INVALID_ARGUMENT
+    need = P.moe_workspace_size(d, P.MOE_WS_PERMUTE)
+    with pytest.raises(P.MoeError) as ei:
+        P.moe_permute(d, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need - 1, stream=0)
+    assert ei.value.status == P.MOE_ERR_WORKSPACE_TOO_SMALL
+    with pytest.raises(P.MoeError) as ei:
+        P.moe_expert_ffn_bwd(d, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                             FAKE, 0, stream=0)
+    assert ei.value.status == P.MOE_ERR_WORKSPACE_TOO_SMALL
+    # the router adjoint needs every expert's gate gradient: a party shard is refused
+    shard = desc(n_experts=8, local_begin=0, local_count=4)
+    with pytest.raises(P.MoeError) as ei:
+        P.moe_route_bwd(shard, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, stream=0)
+    assert ei.value.status == P.MOE_ERR_INVALID_ARGUMENT
+
+
+def test_timing_report_empty():
+    P.moe_kernel_timing(False)
+    assert P.moe_kernel_timing_report() == {}

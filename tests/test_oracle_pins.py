@@ -370,6 +370,20 @@ def test_token_pieces_match_layer():
     assert rel(tp["dx_experts"], bwd["dx_experts"][toks]) < 1e-12
 
 
+def test_wgrad_slices_match_layer():
+    cfg = LayerConfig("sl", T=64, d=16, f=24, E=4, k=2, dtype="f32", seed=19)
+    inp = make_inputs(cfg, with_dy=True)
+    fwd = moe_layer.layer_forward(inp)
+    bwd = moe_layer.layer_backward(inp, fwd, inp.dy)
+    for e in range(cfg.n_local):
+        r0, r1 = fwd["offsets"][e], fwd["offsets"][e + 1]
+        sl = moe_layer.expert_wgrad_slices(fwd["xp"][r0:r1], bwd["dO"][r0:r1], inp.w_gate[e], inp.w_up[e],
+                                           inp.w_down[e], [0, 5, 23], [1, 7])
+        assert rel(sl["dW_gate_rows"], bwd["dW_gate"][e][[0, 5, 23]]) < 1e-12
+        assert rel(sl["dW_up_rows"], bwd["dW_up"][e][[0, 5, 23]]) < 1e-12
+        assert rel(sl["dW_down_cols"], bwd["dW_down"][e][:, [1, 7]]) < 1e-12
+
+
 # ----------------------------------------------- planted mistakes: each pin catches its kind
 
 def _fails(pin, *a, **kw):
