@@ -1,0 +1,165 @@
+"""Benchmark of the MoE expert layer (forward + backward) on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2] [--no-cpu-baseline]
+
+One step is one pass of the whole layer over one batch of resident synthetic inputs:
+route -> permute -> expert FFN forward -> combine -> combine backward -> expert FFN backward
+-> router backward -> unpermute. The workload is the bf16 layer T=4096, d=1024, f=2816,
+E=16 SwiGLU experts, top-2 (seeded inputs, weights ~ N(0, 1/fan_in)).
+
+Prints ONE JSON line: the layer's algorithmic TFLOP/s (6*d*f per routed-or-shared row forward,
+12*d*f backward, 2*T*d*E router forward, 4*T*d*E router backward), tokens/s, the roofline of the
+dominant kernel measured with HIP events on the library's stream during the timed steps, and the
+CPU oracle's throughput on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+BF16_PEAK_TFLOPS = 2516.6      # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 FLOP/clk
+FP32_PEAK_TFLOPS = 157.3       # MI355X fp32 matrix
+HBM_PEAK_GBS = 8000.0
+
+# algorithmic FLOPs of each kernel per launch, per routed-or-shared row (x d*f)
+GEMM_FLOPS_PER_ROW_DF = {
+    "gemm_fwd_gate_up": 4.0, "gemm_fwd_down": 2.0, "gemm_bwd_dh": 2.0, "gemm_wgrad_down": 2.0,
+    "gemm_wgrad_gate_up": 4.0, "gemm_bwd_dx": 4.0,
+}
+
+
+def layer_flops(cfg, n_routed_rows, backward=True):
+    rows = n_routed_rows + cfg.n_shared * cfg.T
+    fl = 6.0 * cfg.d * cfg.f * rows + 2.0 * cfg.T * cfg.d * cfg.E
+    if backward:
+        fl += 12.0 * cfg.d * cfg.f * rows
+        if cfg.router_backward:
+            fl += 4.0 * cfg.T * cfg.d * cfg.E
+    return fl
+
+
+def cpu_baseline(cfg, inp, min_seconds=10.0, max_seconds=30.0):
+    """The CPU oracle (fp64 numpy) on this host's cores, timed on a bounded sample of the workload:
+    whole forward + backward passes of the layer, repeated until about min_seconds of CPU work
+    (first pass always counted; no new pass starts beyond max_seconds)."""
+    from oracle import moe_layer as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    n_pass, total, n_rows = 0, 0.0, 0
+    while True:
+        t0 = time.perf_counter()
+        fwd = O.layer_forward(inp)
+        O.layer_backward(inp, fwd, inp.dy)
+        total += time.perf_counter() - t0
+        n_pass += 1
+        n_rows = len(fwd["row_to_slot"])
+        if total >= min_seconds or total * (n_pass + 1) / n_pass > max_seconds:
+            break
+    dt = total / n_pass
+    fl = layer_flops(cfg, n_rows, True)
+    return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n_pass} whole fwd+bwd pass(es) of the workload ({cfg.T} tokens), fp64 numpy, "
+                      f"{total:.1f} s in total", "tokens_per_s": round(cfg.T / dt, 2), "seconds_per_pass": round(dt, 3)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: the layer is one party's shard on one MI355X; "
+              "multi-GPU expert sharding is not built", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2506_02965_amd import pcmoe as P
+    from paper_2506_02965_amd.layer import MoELayer, upload
+    from paper_2506_02965_amd.synth import CONFIGS, make_inputs
+
+    P.lib()
+    cfg = CONFIGS[args.config]
+    inp = make_inputs(cfg, with_dy=True)
+    w = upload(inp, device="cuda")
+    layer = MoELayer(cfg, backward=True)
+
+    def step():
+        layer.forward(w)
+        layer.backward(w)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    n_routed = layer.n_local_rows()
+
+    P.moe_kernel_timing(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / args.steps
+    kt = P.moe_kernel_timing_report()
+    P.moe_kernel_timing(False)
+
+    flops = layer_flops(cfg, n_routed, True)
+    tflops = flops / dt / 1e12
+    rows = n_routed + cfg.n_shared * cfg.T
+    # dominant kernel: largest total time among the recorded launches
+    dom = max(kt.items(), key=lambda kv: kv[1][1])
+    dom_name, (dom_cnt, dom_ms) = dom
+    dom_avg_s = dom_ms / dom_cnt / 1e3
+    kernels = {k: {"launches_per_step": c / args.steps, "avg_us": ms / c * 1e3} for k, (c, ms) in kt.items()}
+    if dom_name in GEMM_FLOPS_PER_ROW_DF:
+        per_launch = GEMM_FLOPS_PER_ROW_DF[dom_name] * cfg.d * cfg.f * rows
+        ach = per_launch / dom_avg_s / 1e12
+        peak = BF16_PEAK_TFLOPS if cfg.dtype == "bf16" else FP32_PEAK_TFLOPS
+        roof = {"kernel": dom_name, "bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(ach / peak, 4), "traffic": None,
+                "algorithmic_per_launch": per_launch, "avg_launch_us": round(dom_avg_s * 1e6, 2)}
+    else:
+        roof = {"kernel": dom_name, "bound": None, "achieved": None, "peak": None, "unit": None, "frac": None,
+                "traffic": None, "avg_launch_us": round(dom_avg_s * 1e6, 2)}
+    gemm_us = sum(v["avg_us"] * v["launches_per_step"] for k, v in kernels.items() if k.startswith("gemm_"))
+    out = {
+        "metric": "MoE-layer fwd+bwd TFLOP/s and tokens/s; % of MI355X bf16 MFMA peak",
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(dt * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded N(0,1) activations, N(0,1/fan_in) weights)",
+        "config": {"workload": cfg.name, "T": cfg.T, "d_model": cfg.d, "d_ff": cfg.f, "E": cfg.E, "top_k": cfg.k,
+                   "n_shared": cfg.n_shared, "hosted_experts": cfg.n_local, "routed_rows": n_routed,
+                   "parallelism": "single GPU"},
+        "tokens_per_s": round(cfg.T / dt, 1),
+        "pct_bf16_peak": round(100.0 * tflops / BF16_PEAK_TFLOPS, 3),
+        "expert_gemm_tflops": round((18.0 * cfg.d * cfg.f * rows) / (gemm_us * 1e-6) / 1e12, 2) if gemm_us else None,
+        "roofline": roof,
+        "kernels": {k: {"avg_us": round(v["avg_us"], 2), "per_step": v["launches_per_step"]}
+                    for k, v in kernels.items()},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, inp)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
