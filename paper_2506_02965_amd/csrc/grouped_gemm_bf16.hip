@@ -1,0 +1,556 @@
+// Expert passes of Alg. 6 (ForwardExpert / BackwardExpert) as grouped bf16 GEMMs on CDNA4 MFMA.
+//
+// Same six contractions as the fp32 path (see grouped_gemm.h), built for gfx950:
+//   * operands stream global -> LDS with direct-to-LDS buffer loads (16 bytes per lane, no VGPR
+//     staging) through a STAGES-deep ring of LDS buffers, so STAGES-1 K-tiles are in flight while
+//     the MFMAs consume one; rows past a group's end read as zeros through the buffer range check;
+//   * K-contiguous operands sit in LDS as 128-byte rows with a 16-byte-chunk XOR swizzle and feed
+//     v_mfma_f32_16x16x32_bf16 through pairs of ds_read_b64 (measured faster than ds_read_b128 on
+//     gfx950 when odd lane groups read their upper half first);
+//   * operands whose K is the slow dimension (W_down / W_{gate,up} in the input gradients, both
+//     operands of the weight gradients) stay in their natural [k][mn] layout and are transposed on
+//     the way into registers by ds_read_b64_tr_b16 (two reads per MFMA operand);
+//   * four wavefronts (2 x 2) per workgroup, fp32 accumulators in AGPR/VGPRs, per-wave epilogue
+//     staged through LDS in fp32 and written as 16-byte chunks (SwiGLU and its adjoint fused).
+#include "grouped_gemm.h"
+
+#include <cstdlib>
+#include <cstring>
+
+namespace pcmoe {
+
+typedef int int32x4 __attribute__((ext_vector_type(4)));
+typedef short short4v __attribute__((ext_vector_type(4)));
+
+extern "C" __device__ void llvm_amdgcn_raw_buffer_load_lds(int32x4 rsrc, __attribute__((address_space(3))) uint32_t* lds,
+                                                           int size, int voffset, int soffset, int offset, int aux)
+    __asm("llvm.amdgcn.raw.buffer.load.lds");
+
+// Buffer resource over [base, base + bytes): loads at offsets >= bytes return zeros.
+__device__ __forceinline__ int32x4 make_rsrc(const void* base, uint32_t bytes) {
+  struct {
+    const void* p;
+    uint32_t range;
+    uint32_t cfg;
+  } r = {base, bytes, 0x00020000u};
+  int32x4 v = __builtin_bit_cast(int32x4, r);
+  v.x = __builtin_amdgcn_readfirstlane(v.x);
+  v.y = __builtin_amdgcn_readfirstlane(v.y);
+  v.z = __builtin_amdgcn_readfirstlane(v.z);
+  v.w = __builtin_amdgcn_readfirstlane(v.w);
+  return v;
+}
+
+__device__ __forceinline__ void dma16(int32x4 rsrc, char* lds_dst, int voff) {
+  llvm_amdgcn_raw_buffer_load_lds(rsrc, (__attribute__((address_space(3))) uint32_t*)lds_dst, 16, voff, 0, 0, 0);
+}
+
+// K-contiguous tile rows of BK bf16 (BK = 64: 8 chunks of 16 bytes; BK = 32: 4 chunks): chunk c of row r
+// lives at chunk c ^ kc_swz(r). With the two 8-byte halves read by alternating lane groups, 16 rows of
+// one chunk column then cover every bank once per LDS pass.
+template <int BK>
+__device__ __forceinline__ int kc_swz(int r) {
+  if (BK == 64) return (r ^ (r >> 3)) & 7;
+  return (r >> 2) & 3;
+}
+// K-major tile rows (R*2 bytes): 16-byte chunk c of k-row k lives at chunk c ^ mc_swz(k).
+__device__ __forceinline__ int mc_swz(int k) { return ((k & 3) << 1) | (((k >> 3) & 1) << 3); }
+
+// A K-contiguous operand fragment as two 8-byte reads. Lane groups with odd q read the upper half of
+// their 16-byte chunk first, so that the 32 lanes of one LDS pass cover all banks; the MFMA then sees
+// k-elements 4..7 before 0..3 in those lanes, and the partner operand is read in the same order.
+__device__ __forceinline__ Chunk lds_kc_pair(const char* chunk, int q) {
+  const int h = (q & 1) * 8;
+  const uint2 a = *reinterpret_cast<const uint2*>(chunk + h);
+  const uint2 b = *reinterpret_cast<const uint2*>(chunk + (8 - h));
+  Chunk c;
+  c.w[0] = a.x;
+  c.w[1] = a.y;
+  c.w[2] = b.x;
+  c.w[3] = b.y;
+  return c;
+}
+
+__device__ __forceinline__ Chunk lds_tr_pair(const char* a0, const char* a1) {
+  typedef __attribute__((address_space(3))) short4v* lp;
+  short4v r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lp)(a0));
+  short4v r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lp)(a1));
+  Chunk c;
+  c.w[0] = (uint32_t)(uint16_t)r0[0] | ((uint32_t)(uint16_t)r0[1] << 16);
+  c.w[1] = (uint32_t)(uint16_t)r0[2] | ((uint32_t)(uint16_t)r0[3] << 16);
+  c.w[2] = (uint32_t)(uint16_t)r1[0] | ((uint32_t)(uint16_t)r1[1] << 16);
+  c.w[3] = (uint32_t)(uint16_t)r1[2] | ((uint32_t)(uint16_t)r1[3] << 16);
+  return c;
+}
+
+__device__ __forceinline__ void mfma_bf16(floatx4& acc, const Chunk& a, const Chunk& b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), acc, 0,
+                                                0, 0);
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+template <int BM, int BN, int BK, int STAGES, int WM, int WN>
+struct Cfg2 {
+  static constexpr int NW = WM * WN;
+  static constexpr int NT = 64 * NW;
+  static constexpr int WTM = BM / WM, WTN = BN / WN;
+  static constexpr int FM = WTM / 16, FN = WTN / 16;
+  static constexpr int ROWB = BK * 2;              // bytes of one K-contiguous tile row
+  static constexpr int CR = ROWB / 16;             // 16-byte chunks per K-contiguous row
+  static constexpr int RPI = 1024 / ROWB;          // K-contiguous rows per direct-load instruction
+  static constexpr int KK = BK / 32;               // MFMA k-steps per K-tile
+  static constexpr int STAGE_BYTES = (BM + BN) * ROWB;
+  static constexpr int LDS_MAIN = STAGES * STAGE_BYTES;
+  static constexpr int PART_ROWS = WTM < 32 ? WTM : 32;
+  static constexpr int PITCH = WTN + 4;  // fp32 epilogue staging pitch
+  static constexpr int WAVE_EPI = PART_ROWS * PITCH * 4;
+  static constexpr int LDS_EPI = NW * WAVE_EPI;
+  static constexpr int LDS = LDS_MAIN > LDS_EPI ? LDS_MAIN : LDS_EPI;
+  static constexpr int IA = BM * ROWB / 1024 / NW;  // direct loads per wave per K-tile (1 KB each)
+  static constexpr int IB = BN * ROWB / 1024 / NW;
+  static constexpr int LOADS = IA + IB;
+  static_assert(IA * 1024 * NW == BM * ROWB && IB * 1024 * NW == BN * ROWB, "tiles must split evenly over waves");
+};
+
+template <int BM, int BN, int BK, int KIND, int STAGES, int WM, int WN>
+__global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs p) {
+  using C = Cfg2<BM, BN, BK, STAGES, WM, WN>;
+  using KT = KindTraits<KIND>;
+  constexpr int ES = 2;
+  extern __shared__ __align__(16) char smem[];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (LDS DMA bases, resources)
+  const int wm = wave / WN, wn = wave % WN;
+
+  TileIdx ti;
+  if (!decode_tile<KT::ragged_m>(p, ti)) return;
+  const int g = ti.g;
+  const int d = p.d, f = p.f;
+  const bool routed = g < p.Eloc;
+  const int row0 = routed ? p.offsets[g] : 0;
+  const int rows = routed ? p.offsets[g + 1] - row0 : p.T;
+  const size_t rs = routed ? (size_t)row0 : (size_t)p.rows_cap + (size_t)(g - p.Eloc) * p.T;
+  const int m0 = ti.mt * BM, n0 = ti.nt * BN;
+  int K;
+  if (KIND == FWD_GU || KIND == BWD_DH) K = d;
+  else if (KIND == FWD_DOWN) K = f;
+  else if (KIND == BWD_DX) K = 2 * f;
+  else K = rows;
+
+  // ------------------------------------------------------------------ operand sources
+  // A (M side). Ragged kinds: K-contiguous rows of the group; weight gradients: [rows][M] (K-major).
+  int32x4 ra;
+  int a_ld;  // bytes between consecutive rows in memory
+  {
+    const char* base;
+    if (KIND == FWD_GU) { base = routed ? (const char*)p.xp + rs * d * ES : (const char*)p.x; a_ld = d * ES; }
+    else if (KIND == FWD_DOWN) { base = (const char*)p.h + rs * f * ES; a_ld = f * ES; }
+    else if (KIND == BWD_DH || KIND == WG_DOWN) {
+      base = routed ? (const char*)p.dyp + rs * d * ES : (const char*)p.dy;
+      a_ld = d * ES;
+    } else { base = (const char*)p.dgu + rs * 2 * f * ES; a_ld = 2 * f * ES; }
+    ra = make_rsrc(base, (uint32_t)((size_t)rows * a_ld));
+  }
+  // B (N side)
+  int32x4 rb0, rb1;  // rb1: W_up (FWD_GU rows of the up half; BWD_DX K rows >= f)
+  int b_ld;
+  if (KIND == FWD_GU) {
+    rb0 = make_rsrc((const char*)p.wg + (size_t)g * f * d * ES, (uint32_t)((size_t)f * d * ES));
+    rb1 = make_rsrc((const char*)p.wu + (size_t)g * f * d * ES, (uint32_t)((size_t)f * d * ES));
+    b_ld = d * ES;
+  } else if (KIND == FWD_DOWN || KIND == BWD_DH) {
+    rb0 = make_rsrc((const char*)p.wd + (size_t)g * d * f * ES, (uint32_t)((size_t)d * f * ES));
+    rb1 = rb0;
+    b_ld = f * ES;
+  } else if (KIND == BWD_DX) {
+    rb0 = make_rsrc((const char*)p.wg + (size_t)g * f * d * ES, (uint32_t)((size_t)f * d * ES));
+    rb1 = make_rsrc((const char*)p.wu + (size_t)g * f * d * ES, (uint32_t)((size_t)f * d * ES));
+    b_ld = d * ES;
+  } else if (KIND == WG_DOWN) {
+    rb0 = make_rsrc((const char*)p.h + rs * f * ES, (uint32_t)((size_t)rows * f * ES));
+    rb1 = rb0;
+    b_ld = f * ES;
+  } else {  // WG_GU
+    const char* base = routed ? (const char*)p.xp + rs * d * ES : (const char*)p.x;
+    rb0 = make_rsrc(base, (uint32_t)((size_t)rows * d * ES));
+    rb1 = rb0;
+    b_ld = d * ES;
+  }
+
+  // per-lane byte offsets of each direct-load instruction at K-tile 0
+  int va[C::IA], vb[C::IB];
+  bool bup[C::IB];  // FWD_GU: instruction reads W_up rows
+#pragma unroll
+  for (int j = 0; j < C::IA; ++j) {
+    const int jj = wave + C::NW * j;
+    if (KT::a_kc) {
+      const int r = C::RPI * jj + lane / C::CR, c = (lane % C::CR) ^ kc_swz<BK>(r);
+      va[j] = (m0 + r) * a_ld + 16 * c;
+    } else {
+      constexpr int CPR = BM / 8;
+      const int slot = 64 * jj + lane, kr = slot / CPR, c = (slot % CPR) ^ mc_swz(kr);
+      va[j] = kr * a_ld + (m0 + 8 * c) * ES;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < C::IB; ++j) {
+    const int jj = wave + C::NW * j;
+    bup[j] = false;
+    if (KT::b_kc) {
+      const int r = C::RPI * jj + lane / C::CR, c = (lane % C::CR) ^ kc_swz<BK>(r);
+      int wrow;
+      if (KIND == FWD_GU) {
+        const int wcol = r / C::WTN, within = r % C::WTN, half = C::WTN / 2;
+        static_assert((C::WTN / 2) % C::RPI == 0, "a direct load must not straddle gate and up rows");
+        wrow = ti.nt * (BN / 2) + wcol * half + (within % half);
+        bup[j] = ((C::RPI * jj) % C::WTN) >= half;  // the instruction's rows are all gate or all up rows
+      } else {
+        wrow = n0 + r;
+      }
+      vb[j] = wrow * b_ld + 16 * c;
+    } else {
+      constexpr int CPR = BN / 8;
+      const int slot = 64 * jj + lane, kr = slot / CPR, c = (slot % CPR) ^ mc_swz(kr);
+      vb[j] = kr * b_ld + (n0 + 8 * c) * ES;
+    }
+  }
+
+  // Direct load number idx (0 .. LOADS-1) of K-tile kt into LDS stage `stage`.
+  auto issue_one = [&](int kt, int stage, int idx) {
+    char* As = smem + stage * C::STAGE_BYTES;
+    char* Bs = As + BM * C::ROWB;
+    const int k0 = kt * BK;
+    if (idx < C::IA) {
+      const int j = idx;
+      dma16(ra, As + (wave + C::NW * j) * 1024, va[j] + (KT::a_kc ? k0 * ES : k0 * a_ld));
+    } else {
+      const int j = idx - C::IA;
+      if (KIND == BWD_DX) {
+        const bool up = k0 >= f;
+        dma16(up ? rb1 : rb0, Bs + (wave + C::NW * j) * 1024, vb[j] + (up ? k0 - f : k0) * b_ld);
+      } else {
+        dma16(bup[j] ? rb1 : rb0, Bs + (wave + C::NW * j) * 1024, vb[j] + (KT::b_kc ? k0 * ES : k0 * b_ld));
+      }
+    }
+  };
+  auto issue = [&](int kt, int stage) {
+#pragma unroll
+    for (int idx = 0; idx < C::LOADS; ++idx) issue_one(kt, stage, idx);
+  };
+
+  floatx4 acc[C::FM][C::FN];
+#pragma unroll
+  for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  const int KTN = (K + BK - 1) / BK;
+  // prologue: STAGES-1 tiles in flight
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < KTN) issue(s, s);
+
+  const int q = lane >> 4, li = lane & 15;
+  for (int kt = 0; kt < KTN; ++kt) {
+    // tile kt has landed when at most the later tiles' loads are outstanding
+    if (kt + STAGES - 2 < KTN) wait_vmcnt<(STAGES - 2) * C::LOADS>();
+    else wait_vmcnt<0>();
+    __syncthreads();
+    if (kt + STAGES - 1 < KTN) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
+    const char* As = smem + (kt % STAGES) * C::STAGE_BYTES;
+    const char* Bs = As + BM * C::ROWB;
+#pragma unroll
+    for (int kk = 0; kk < C::KK; ++kk) {
+      Chunk a[C::FM], b[C::FN];
+#pragma unroll
+      for (int i = 0; i < C::FM; ++i) {
+        if (KT::a_kc) {
+          const int r = wm * C::WTM + 16 * i + li, c = 4 * kk + q;
+          a[i] = lds_kc_pair(As + r * C::ROWB + ((c ^ kc_swz<BK>(r)) << 4), q);
+        } else {
+          const int k1 = 32 * kk + 8 * q + 4 * (q & 1) + (li >> 2), mn = wm * C::WTM + 16 * i + 4 * (li & 3);
+          const int k2 = k1 + 4 - 8 * (q & 1);
+          a[i] = lds_tr_pair(As + k1 * (BM * 2) + (((mn >> 3) ^ mc_swz(k1)) << 4) + (mn & 7) * 2,
+                             As + k2 * (BM * 2) + (((mn >> 3) ^ mc_swz(k2)) << 4) + (mn & 7) * 2);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < C::FN; ++j) {
+        if (KT::b_kc) {
+          const int r = wn * C::WTN + 16 * j + li, c = 4 * kk + q;
+          b[j] = lds_kc_pair(Bs + r * C::ROWB + ((c ^ kc_swz<BK>(r)) << 4), q);
+        } else {
+          const int k1 = 32 * kk + 8 * q + 4 * (q & 1) + (li >> 2), mn = wn * C::WTN + 16 * j + 4 * (li & 3);
+          const int k2 = k1 + 4 - 8 * (q & 1);
+          b[j] = lds_tr_pair(Bs + k1 * (BN * 2) + (((mn >> 3) ^ mc_swz(k1)) << 4) + (mn & 7) * 2,
+                             Bs + k2 * (BN * 2) + (((mn >> 3) ^ mc_swz(k2)) << 4) + (mn & 7) * 2);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j) mfma_bf16(acc[i][j], a[i], b[j]);
+    }
+  }
+  __syncthreads();  // every wave is done with the operand buffers
+
+  // ------------------------------------------------------------------ epilogue (per wave)
+  float* st = reinterpret_cast<float*>(smem + wave * C::WAVE_EPI);
+  constexpr int FPP = C::PART_ROWS / 16;  // fm blocks per part
+  constexpr int OUT_W = (KIND == FWD_GU) ? C::WTN / 2 : C::WTN;  // output columns of the wave
+  constexpr int CPRW = OUT_W / 8;                                  // 16-byte output chunks per row
+#pragma unroll
+  for (int part = 0; part < C::FM / FPP; ++part) {
+#pragma unroll
+    for (int i = 0; i < FPP; ++i)
+#pragma unroll
+      for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) st[(16 * i + 4 * q + r) * C::PITCH + 16 * j + li] = acc[part * FPP + i][j][r];
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's staging writes are done
+    __builtin_amdgcn_wave_barrier();
+    for (int qq = lane; qq < C::PART_ROWS * CPRW; qq += 64) {
+      const int rr = qq / CPRW, cc = (qq % CPRW) * 8;
+      const int m = m0 + wm * C::WTM + part * C::PART_ROWS + rr;
+      if (KT::ragged_m && m >= rows) continue;
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = st[rr * C::PITCH + cc + e];
+      if (KIND == FWD_GU) {
+        float u[8], hv[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          u[e] = st[rr * C::PITCH + OUT_W + cc + e];
+          const float sg = 1.f / (1.f + __expf(-v[e]));
+          hv[e] = v[e] * sg * u[e];
+        }
+        const int col = ti.nt * (BN / 2) + wn * OUT_W + cc;
+        char* gu = (char*)p.gu + ((rs + m) * 2 * f + col) * ES;
+        st_chunk(gu, f_to_chunk<bf16>(v));
+        st_chunk(gu + (size_t)f * ES, f_to_chunk<bf16>(u));
+        st_chunk((char*)p.h + ((rs + m) * f + col) * ES, f_to_chunk<bf16>(hv));
+      } else if (KIND == FWD_DOWN || KIND == BWD_DX) {
+        st_chunk((char*)p.out + ((rs + m) * d + n0 + wn * OUT_W + cc) * ES, f_to_chunk<bf16>(v));
+      } else if (KIND == BWD_DH) {
+        const int col = n0 + wn * OUT_W + cc;
+        const char* gu = (const char*)p.gu + ((rs + m) * 2 * f + col) * ES;
+        float gv[8], uv[8], dg[8], du[8];
+        chunk_to_f<bf16>(ld_chunk(gu), gv);
+        chunk_to_f<bf16>(ld_chunk(gu + (size_t)f * ES), uv);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float sg = 1.f / (1.f + __expf(-gv[e]));
+          du[e] = v[e] * gv[e] * sg;
+          dg[e] = v[e] * uv[e] * sg * (1.f + gv[e] * (1.f - sg));
+        }
+        char* o = (char*)p.dgu + ((rs + m) * 2 * f + col) * ES;
+        st_chunk(o, f_to_chunk<bf16>(dg));
+        st_chunk(o + (size_t)f * ES, f_to_chunk<bf16>(du));
+      } else if (KIND == WG_DOWN) {
+        st_chunk((char*)p.out + (((size_t)g * d + m) * f + n0 + wn * OUT_W + cc) * ES, f_to_chunk<bf16>(v));
+      } else {  // WG_GU
+        const int col = n0 + wn * OUT_W + cc;
+        char* o = (m < f) ? (char*)p.out + (((size_t)g * f + m) * d + col) * ES
+                          : (char*)p.out2 + (((size_t)g * f + (m - f)) * d + col) * ES;
+        st_chunk(o, f_to_chunk<bf16>(v));
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+// ------------------------------------------------------------------------- host side
+
+template <int BM, int BN, int BK, int KIND, int STAGES, int WM, int WN>
+static hipError_t run2(const GemmArgs& a, long tiles, hipStream_t s, const char* name) {
+  using C = Cfg2<BM, BN, BK, STAGES, WM, WN>;
+  static_assert(C::LDS <= 160 * 1024, "LDS budget of one CU");
+  auto kern = gemm_bf16_kernel<BM, BN, BK, KIND, STAGES, WM, WN>;
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  const int grid = (int)((tiles + 7) / 8 * 8);
+  if (grid <= 0) return hipSuccess;
+  KernelTimer kt(name, s);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(C::NT), C::LDS, s, a);
+  return hipGetLastError();
+}
+
+// Tile shapes (BM x BN, LDS stages, wavefronts) instantiated for every contraction. Two wavefronts
+// per SIMD are what keep the MFMA pipes busy: 4-wave 128x128 tiles run two workgroups per CU,
+// the larger tiles use 8 wavefronts in one workgroup.
+enum TileShape { T128x128s2 = 0, T256x128w8, T128x256w8, T256x256w8, T256x256k32, T256x128k32, T128x128k32,
+                 T256x256w16, N_SHAPES };
+static const int kShapeBM[N_SHAPES] = {128, 256, 128, 256, 256, 256, 128, 256};
+static const int kShapeBN[N_SHAPES] = {128, 128, 256, 256, 256, 128, 128, 256};
+static const char* kShapeName[N_SHAPES] = {"128x128s2", "256x128w8", "128x256w8", "256x256w8", "256x256k32",
+                                           "256x128k32", "128x128k32", "256x256w16"};
+
+static const char* kKindName[6] = {"gemm_fwd_gate_up", "gemm_fwd_down", "gemm_bwd_dh", "gemm_bwd_dx",
+                                   "gemm_wgrad_down", "gemm_wgrad_gate_up"};
+
+template <int KIND>
+static hipError_t run_shape(int shape, const GemmArgs& a, long tiles, hipStream_t s) {
+  switch (shape) {
+    case T128x128s2: return run2<128, 128, 64, KIND, 2, 2, 2>(a, tiles, s, kKindName[KIND]);
+    case T256x128w8: return run2<256, 128, 64, KIND, 2, 4, 2>(a, tiles, s, kKindName[KIND]);
+    case T128x256w8: return run2<128, 256, 64, KIND, 2, 2, 4>(a, tiles, s, kKindName[KIND]);
+    case T256x256k32: return run2<256, 256, 32, KIND, 4, 2, 4>(a, tiles, s, kKindName[KIND]);
+    case T256x128k32: return run2<256, 128, 32, KIND, 4, 4, 2>(a, tiles, s, kKindName[KIND]);
+    case T128x128k32: return run2<128, 128, 32, KIND, 3, 2, 2>(a, tiles, s, kKindName[KIND]);
+    case T256x256w16: return run2<256, 256, 64, KIND, 2, 4, 4>(a, tiles, s, kKindName[KIND]);
+    default: return run2<256, 256, 64, KIND, 2, 2, 4>(a, tiles, s, kKindName[KIND]);
+  }
+}
+
+// Default shape per contraction; PCMOE_GEMM_TILES="<kind>=<shape>,..." overrides (kind 0..5 as in
+// GemmKind, shape as in kShapeName), e.g. "0=256x256s2,5=128x256s3".
+static int tile_shape(int kind, const moe_desc& d) {
+  static int table[6] = {-1, -1, -1, -1, -1, -1};
+  static bool parsed = false;
+  if (!parsed) {
+    parsed = true;
+    if (const char* env = getenv("PCMOE_GEMM_TILES")) {
+      const char* p = env;
+      while (*p) {
+        int k = *p - '0';
+        if (k >= 0 && k < 6 && p[1] == '=') {
+          for (int sh = 0; sh < N_SHAPES; ++sh)
+            if (!strncmp(p + 2, kShapeName[sh], strlen(kShapeName[sh]))) table[k] = sh;
+        }
+        while (*p && *p != ',') ++p;
+        if (*p == ',') ++p;
+      }
+    }
+  }
+  if (table[kind] >= 0) return table[kind];
+  (void)d;
+  return T128x128s2;
+}
+
+// Upper bound on the m-tiles of the row-ragged kinds (per-expert counts stay on the device).
+static long mtile_bound2(const moe_desc& d, int bm) {
+  long routed = ((long)d.T * d.top_k + (long)d.local_count * (bm - 1)) / bm;
+  return routed + (long)d.n_shared * ((d.T + bm - 1) / bm);
+}
+
+size_t ffn_saved_bytes(const moe_desc& d) {
+  const size_t R = (size_t)rows_total(d), es = elem_bytes(d);
+  return align256(R * 2 * d.d_ff * es) + align256(R * d.d_ff * es);
+}
+static size_t plan_part(const moe_desc& d) { return align256((size_t)(d.local_count + d.n_shared + 1) * 4); }
+static size_t plan_bytes(const moe_desc& d) { return 3 * plan_part(d); }
+size_t ffn_fwd_ws_bytes(const moe_desc& d) { return plan_bytes(d); }
+size_t ffn_bwd_ws_bytes(const moe_desc& d) {
+  const size_t R = (size_t)rows_total(d), es = elem_bytes(d);
+  return align256(R * 2 * d.d_ff * es) + plan_bytes(d);
+}
+
+struct Plan {
+  int32_t* pre128;
+  int32_t* pre256;
+  int32_t* order;
+};
+
+// m-tile prefixes for 128- and 256-row tiles and the heaviest-first group order
+static Plan plan(const moe_desc& d, const int32_t* offsets, void* where, hipStream_t s) {
+  Plan pl;
+  pl.pre128 = (int32_t*)where;
+  pl.pre256 = (int32_t*)((char*)where + plan_part(d));
+  pl.order = (int32_t*)((char*)where + 2 * plan_part(d));
+  KernelTimer kt("ffn_plan", s);
+  hipLaunchKernelGGL(mtile_prefix_kernel, dim3(1), dim3(512), 0, s, offsets, d.local_count, d.n_shared, d.T, 128, 256,
+                     pl.pre128, pl.pre256, pl.order);
+  return pl;
+}
+
+static GemmArgs args_for(const moe_desc& d, const int32_t* offsets) {
+  GemmArgs a{};
+  a.T = d.T; a.k = d.top_k; a.d = d.d_model; a.f = d.d_ff; a.Eloc = d.local_count; a.S = d.n_shared;
+  a.rows_cap = d.T * d.top_k;
+  a.offsets = offsets;
+  return a;
+}
+
+// Ragged-M contraction: n_cols output columns of the tile grid (FWD_GU: gate columns, two per pair).
+// A shape must tile M and N exactly (d_model, d_ff are multiples of 128): fall back to 128-wide sides.
+static int fit_shape(int sh, int M, int N) {
+  int bm = kShapeBM[sh], bn = kShapeBN[sh];
+  if (M > 0 && M % bm) bm = 128;
+  if (N % bn) bn = 128;
+  if (bm == kShapeBM[sh] && bn == kShapeBN[sh]) return sh;
+  const bool k32 = sh == T256x256k32 || sh == T256x128k32 || sh == T128x128k32;
+  if (sh == T256x256w16 && bn == 128) return bm == 256 ? T256x128w8 : T128x128s2;
+  if (bm == 256 && bn == 128) return k32 ? T256x128k32 : T256x128w8;
+  if (bm == 128 && bn == 256) return T128x256w8;
+  return k32 ? T128x128k32 : T128x128s2;
+}
+
+template <int KIND>
+static hipError_t ragged(const moe_desc& d, GemmArgs a, const Plan& pl, int n_cols, hipStream_t s) {
+  const int sh = fit_shape(tile_shape(KIND, d), 0, n_cols);
+  const int bm = kShapeBM[sh], bn = kShapeBN[sh];
+  a.mt_prefix = bm == 128 ? pl.pre128 : pl.pre256;
+  a.n_tiles = n_cols / bn;  // FWD_GU: n_cols = 2f, each tile holds bn/2 gate and bn/2 up columns
+  return run_shape<KIND>(sh, a, mtile_bound2(d, bm) * a.n_tiles, s);
+}
+
+template <int KIND>
+static hipError_t wgrad(const moe_desc& d, GemmArgs a, const Plan& pl, int M, int N, hipStream_t s) {
+  const int sh = fit_shape(tile_shape(KIND, d), M, N);
+  a.order = pl.order;
+  a.m_tiles = M / kShapeBM[sh];
+  a.n_tiles = N / kShapeBN[sh];
+  return run_shape<KIND>(sh, a, (long)(d.local_count + d.n_shared) * a.m_tiles * a.n_tiles, s);
+}
+
+hipError_t launch_ffn_fwd(const moe_desc& d, const void* x, const void* xp, const int32_t* offsets, const void* wg,
+                          const void* wu, const void* wd, void* yp, void* saved, void* ws, hipStream_t s) {
+  Plan pl = plan(d, offsets, ws, s);
+  if (d.dtype != MOE_BF16) return ffn_fwd_f32(d, x, xp, offsets, wg, wu, wd, yp, saved, pl.pre128, s);
+  const size_t R = (size_t)rows_total(d);
+  GemmArgs a = args_for(d, offsets);
+  a.x = x; a.xp = xp; a.wg = wg; a.wu = wu; a.wd = wd;
+  a.gu = saved;
+  a.h = (char*)saved + align256(R * 2 * d.d_ff * 2);
+  a.out = yp;
+  hipError_t e;
+  if ((e = ragged<FWD_GU>(d, a, pl, 2 * d.d_ff, s)) != hipSuccess) return e;
+  if ((e = ragged<FWD_DOWN>(d, a, pl, d.d_model, s)) != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+hipError_t launch_ffn_bwd(const moe_desc& d, const void* x, const void* xp, const void* dy, const void* dyp,
+                          const int32_t* offsets, const void* wg, const void* wu, const void* wd, const void* saved,
+                          void* dxp, void* dwg, void* dwu, void* dwd, void* ws, hipStream_t s) {
+  const size_t R = (size_t)rows_total(d), es = elem_bytes(d);
+  void* dgu = ws;
+  Plan pl = plan(d, offsets, (char*)ws + align256(R * 2 * d.d_ff * es), s);
+  if (d.dtype != MOE_BF16)
+    return ffn_bwd_f32(d, x, xp, dy, dyp, offsets, wg, wu, wd, saved, dxp, dwg, dwu, dwd, dgu, pl.pre128, s);
+  GemmArgs a = args_for(d, offsets);
+  a.x = x; a.xp = xp; a.dy = dy; a.dyp = dyp; a.wg = wg; a.wu = wu; a.wd = wd;
+  a.gu = (void*)saved;
+  a.h = (char*)saved + align256(R * 2 * d.d_ff * 2);
+  a.dgu = dgu;
+  hipError_t e;
+  if ((e = ragged<BWD_DH>(d, a, pl, d.d_ff, s)) != hipSuccess) return e;
+  a.out = dwd;
+  if ((e = wgrad<WG_DOWN>(d, a, pl, d.d_model, d.d_ff, s)) != hipSuccess) return e;
+  a.out = dwg;
+  a.out2 = dwu;
+  if ((e = wgrad<WG_GU>(d, a, pl, 2 * d.d_ff, d.d_model, s)) != hipSuccess) return e;
+  a.out = dxp;
+  if ((e = ragged<BWD_DX>(d, a, pl, d.d_model, s)) != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+}  // namespace pcmoe

@@ -1,4 +1,5 @@
-// Expert passes of Alg. 6 (ForwardExpert / BackwardExpert) as grouped GEMMs on MFMA.
+// Expert passes of Alg. 6 (ForwardExpert / BackwardExpert) as grouped GEMMs — fp32 storage path
+// (v_mfma_f32_16x16x4_f32, register-staged double buffer). The bf16 path is grouped_gemm_bf16.hip.
 //
 // One kernel template covers the six contractions of a SwiGLU expert:
 //   FWD_GU   [G|U] = h W_{gate|up}^T, epilogue H = silu(G) * U    (M = rows, N = 2f, K = d)
@@ -14,31 +15,9 @@
 // Operands whose K dimension is not contiguous in memory are transposed in registers on their
 // way to LDS (8x8 blocks of bf16 / 4x4 of fp32), so the MFMA side always reads K-contiguous rows.
 // Epilogues stage the fp32 tile through LDS and write 16-byte chunks.
-#include "pcmoe_internal.h"
+#include "grouped_gemm.h"
 
 namespace pcmoe {
-
-enum GemmKind { FWD_GU = 0, FWD_DOWN = 1, BWD_DH = 2, BWD_DX = 3, WG_DOWN = 4, WG_GU = 5 };
-
-struct GemmArgs {
-  int T, k, d, f, Eloc, S;
-  int rows_cap;               // T*k: first row of the shared experts in the row space
-  const int32_t* offsets;     // [Eloc+1]
-  const int32_t* mt_prefix;   // [G+1] m-tile prefix of the row-ragged kinds
-  int n_tiles, m_tiles;       // tiles along N (all kinds) and along M (weight-gradient kinds)
-  const void* x;              // [T, d]
-  const void* xp;             // [T*k, d]
-  const void* dy;             // [T, d]
-  const void* dyp;            // [T*k, d]
-  const void* wg;             // [G, f, d]
-  const void* wu;             // [G, f, d]
-  const void* wd;             // [G, d, f]
-  void* gu;                   // [R, 2f] saved G|U (FWD_GU writes, BWD_DH reads)
-  void* h;                    // [R, f] saved H
-  void* dgu;                  // [R, 2f] dG|dU
-  void* out;                  // y_perm / dx_perm / dW_down / dW_gate
-  void* out2;                 // dW_up (WG_GU)
-};
 
 __device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 4)) & 7; }
 __device__ __forceinline__ int lds_off(int r, int c) { return r * 128 + ((c ^ swz(r)) << 4); }
@@ -75,16 +54,6 @@ __device__ __forceinline__ void transpose_block(const Chunk* in, Chunk* out, flo
 #pragma unroll
     for (int j = 0; j < 4; ++j) out[m].w[j] = in[j].w[m];
 }
-
-template <int KIND> struct KindTraits;
-template <> struct KindTraits<FWD_GU> { static constexpr bool ragged_m = true, a_kc = true, b_kc = true; };
-template <> struct KindTraits<FWD_DOWN> { static constexpr bool ragged_m = true, a_kc = true, b_kc = true; };
-template <> struct KindTraits<BWD_DH> { static constexpr bool ragged_m = true, a_kc = true, b_kc = false; };
-template <> struct KindTraits<BWD_DX> { static constexpr bool ragged_m = true, a_kc = true, b_kc = false; };
-template <> struct KindTraits<WG_DOWN> { static constexpr bool ragged_m = false, a_kc = false, b_kc = false; };
-template <> struct KindTraits<WG_GU> { static constexpr bool ragged_m = false, a_kc = false, b_kc = false; };
-
-constexpr int GROUP_M = 8;  // m-tiles visited together for L2 reuse of the weight tiles
 
 template <typename T, int BM, int BN, int WM, int WN>
 struct TileCfg {
@@ -159,16 +128,6 @@ struct McLoader {
   }
 };
 
-__device__ __forceinline__ int find_group(const int32_t* __restrict__ pre, int G, int L, int nt) {
-  int lo = 0, hi = G - 1;  // largest g with pre[g]*nt <= L
-  while (lo < hi) {
-    int mid = (lo + hi + 1) >> 1;
-    if (pre[mid] * nt <= L) lo = mid;
-    else hi = mid - 1;
-  }
-  return lo;
-}
-
 template <typename T, int BM, int BN, int WM, int WN, int KIND>
 __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(GemmArgs p) {
   using C = TileCfg<T, BM, BN, WM, WN>;
@@ -177,32 +136,11 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(GemmArgs p) 
   extern __shared__ __align__(16) char smem[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
-  const int G = p.Eloc + p.S;
 
   // ---------------------------------------------------------------- tile decode
-  int total;
-  if (KT::ragged_m) total = p.mt_prefix[G] * p.n_tiles;
-  else total = G * p.m_tiles * p.n_tiles;
-  const int per_xcd = (total + 7) >> 3;
-  const int bid = blockIdx.x;
-  if ((bid >> 3) >= per_xcd) return;
-  const int L = (bid & 7) * per_xcd + (bid >> 3);
-  if (L >= total) return;
-  int g, l, n_mt;
-  if (KT::ragged_m) {
-    g = find_group(p.mt_prefix, G, L, p.n_tiles);
-    l = L - p.mt_prefix[g] * p.n_tiles;
-    n_mt = p.mt_prefix[g + 1] - p.mt_prefix[g];
-  } else {
-    g = L / (p.m_tiles * p.n_tiles);
-    l = L - g * p.m_tiles * p.n_tiles;
-    n_mt = p.m_tiles;
-  }
-  const int mblk = l / (GROUP_M * p.n_tiles);
-  const int rem = l - mblk * GROUP_M * p.n_tiles;
-  const int gsz = min(GROUP_M, n_mt - mblk * GROUP_M);
-  const int nt = rem / gsz;
-  const int mt = mblk * GROUP_M + rem % gsz;
+  TileIdx ti;
+  if (!decode_tile<KT::ragged_m>(p, ti)) return;
+  const int g = ti.g, mt = ti.mt, nt = ti.nt;
 
   const bool routed = g < p.Eloc;
   const int row0 = routed ? p.offsets[g] : 0;                       // first row of the group in its source
@@ -419,26 +357,42 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(GemmArgs p) 
   }
 }
 
-// m-tile prefix over groups: pre[g] = sum_{g' < g} ceil(rows_g' / bm).
+// m-tile prefixes over groups for two tile heights: pre[g] = sum_{g' < g} ceil(rows_g' / bm); and
+// the groups ordered by decreasing row count (ties by index).
 __global__ __launch_bounds__(512) void mtile_prefix_kernel(const int32_t* __restrict__ offsets, int Eloc, int S,
-                                                           int Tn, int bm, int32_t* __restrict__ pre) {
-  __shared__ int buf[2][512];
+                                                           int Tn, int bm0, int bm1, int32_t* __restrict__ pre0,
+                                                           int32_t* __restrict__ pre1, int32_t* __restrict__ order) {
+  __shared__ int buf[2][2][512];
+  __shared__ int rows_s[512];
   const int g = threadIdx.x;
   const int G = Eloc + S;
-  int v = 0;
-  if (g < Eloc) v = (offsets[g + 1] - offsets[g] + bm - 1) / bm;
-  else if (g < G) v = (Tn + bm - 1) / bm;
-  buf[0][g] = v;
+  int rows = 0;
+  if (g < Eloc) rows = offsets[g + 1] - offsets[g];
+  else if (g < G) rows = Tn;
+  buf[0][0][g] = (rows + bm0 - 1) / bm0;
+  buf[1][0][g] = (rows + bm1 - 1) / bm1;
+  rows_s[g] = rows;
   __syncthreads();
+  if (g < G) {
+    int rank = 0;
+    for (int h = 0; h < G; ++h) rank += (rows_s[h] > rows) || (rows_s[h] == rows && h < g);
+    order[rank] = g;
+  }
   int cur = 0;
   for (int off = 1; off < 512; off <<= 1) {
-    int x = buf[cur][g];
-    if (g >= off) x += buf[cur][g - off];
-    buf[cur ^ 1][g] = x;
+#pragma unroll
+    for (int w = 0; w < 2; ++w) {
+      int x = buf[w][cur][g];
+      if (g >= off) x += buf[w][cur][g - off];
+      buf[w][cur ^ 1][g] = x;
+    }
     cur ^= 1;
     __syncthreads();
   }
-  if (g <= G) pre[g] = (g == 0) ? 0 : buf[cur][g - 1];
+  if (g <= G) {
+    pre0[g] = (g == 0) ? 0 : buf[0][cur][g - 1];
+    pre1[g] = (g == 0) ? 0 : buf[1][cur][g - 1];
+  }
 }
 
 // ------------------------------------------------------------------------- host side
@@ -469,16 +423,6 @@ static long mtile_bound(const moe_desc& d) {
   return routed + (long)d.n_shared * ((d.T + T_BM - 1) / T_BM);
 }
 
-size_t ffn_saved_bytes(const moe_desc& d) {
-  const size_t R = (size_t)rows_total(d), es = elem_bytes(d);
-  return align256(R * 2 * d.d_ff * es) + align256(R * d.d_ff * es);
-}
-size_t ffn_fwd_ws_bytes(const moe_desc& d) { return align256((size_t)(d.local_count + d.n_shared + 1) * 4); }
-size_t ffn_bwd_ws_bytes(const moe_desc& d) {
-  const size_t R = (size_t)rows_total(d), es = elem_bytes(d);
-  return align256(R * 2 * d.d_ff * es) + align256((size_t)(d.local_count + d.n_shared + 1) * 4);
-}
-
 static GemmArgs base_args(const moe_desc& d, const int32_t* offsets, const int32_t* pre) {
   GemmArgs a{};
   a.T = d.T; a.k = d.top_k; a.d = d.d_model; a.f = d.d_ff; a.Eloc = d.local_count; a.S = d.n_shared;
@@ -488,16 +432,11 @@ static GemmArgs base_args(const moe_desc& d, const int32_t* offsets, const int32
   return a;
 }
 
-template <typename T>
-static hipError_t ffn_fwd_t(const moe_desc& d, const void* x, const void* xp, const int32_t* offsets, const void* wg,
-                            const void* wu, const void* wd, void* yp, void* saved, void* ws, hipStream_t s) {
+// pre: m-tile prefix for 128-row tiles (computed by the caller's plan launch)
+hipError_t ffn_fwd_f32(const moe_desc& d, const void* x, const void* xp, const int32_t* offsets, const void* wg,
+                       const void* wu, const void* wd, void* yp, void* saved, int32_t* pre, hipStream_t s) {
+  using T = float;
   const size_t R = (size_t)rows_total(d), es = sizeof(T);
-  int32_t* pre = (int32_t*)ws;
-  {
-    KernelTimer kt("ffn_plan", s);
-    hipLaunchKernelGGL(mtile_prefix_kernel, dim3(1), dim3(512), 0, s, offsets, d.local_count, d.n_shared, d.T, T_BM,
-                       pre);
-  }
   GemmArgs a = base_args(d, offsets, pre);
   a.x = x; a.xp = xp; a.wg = wg; a.wu = wu; a.wd = wd;
   a.gu = saved;
@@ -512,18 +451,11 @@ static hipError_t ffn_fwd_t(const moe_desc& d, const void* x, const void* xp, co
   return hipGetLastError();
 }
 
-template <typename T>
-static hipError_t ffn_bwd_t(const moe_desc& d, const void* x, const void* xp, const void* dy, const void* dyp,
-                            const int32_t* offsets, const void* wg, const void* wu, const void* wd, const void* saved,
-                            void* dxp, void* dwg, void* dwu, void* dwd, void* ws, hipStream_t s) {
+hipError_t ffn_bwd_f32(const moe_desc& d, const void* x, const void* xp, const void* dy, const void* dyp,
+                       const int32_t* offsets, const void* wg, const void* wu, const void* wd, const void* saved,
+                       void* dxp, void* dwg, void* dwu, void* dwd, void* dgu, int32_t* pre, hipStream_t s) {
+  using T = float;
   const size_t R = (size_t)rows_total(d), es = sizeof(T);
-  void* dgu = ws;
-  int32_t* pre = (int32_t*)((char*)ws + align256(R * 2 * d.d_ff * es));
-  {
-    KernelTimer kt("ffn_plan", s);
-    hipLaunchKernelGGL(mtile_prefix_kernel, dim3(1), dim3(512), 0, s, offsets, d.local_count, d.n_shared, d.T, T_BM,
-                       pre);
-  }
   GemmArgs a = base_args(d, offsets, pre);
   a.x = x; a.xp = xp; a.dy = dy; a.dyp = dyp; a.wg = wg; a.wu = wu; a.wd = wd;
   a.gu = (void*)saved;
@@ -532,41 +464,23 @@ static hipError_t ffn_bwd_t(const moe_desc& d, const void* x, const void* xp, co
   const long mtb = mtile_bound(d);
   const int G = d.local_count + d.n_shared;
   hipError_t e;
-  // dH -> dG, dU
   a.n_tiles = d.d_ff / T_BN;
   if ((e = run_gemm<T, BWD_DH>(a, round8(mtb * a.n_tiles), s, "gemm_bwd_dh")) != hipSuccess) return e;
-  // dW_down = dO^T H
   a.out = dwd;
   a.m_tiles = d.d_model / T_BM;
   a.n_tiles = d.d_ff / T_BN;
   if ((e = run_gemm<T, WG_DOWN>(a, round8((long)G * a.m_tiles * a.n_tiles), s, "gemm_wgrad_down")) != hipSuccess)
     return e;
-  // [dW_gate; dW_up] = [dG|dU]^T h
   a.out = dwg;
   a.out2 = dwu;
   a.m_tiles = 2 * d.d_ff / T_BM;
   a.n_tiles = d.d_model / T_BN;
   if ((e = run_gemm<T, WG_GU>(a, round8((long)G * a.m_tiles * a.n_tiles), s, "gemm_wgrad_gate_up")) != hipSuccess)
     return e;
-  // dh = [dG|dU] [W_gate; W_up]
   a.out = dxp;
   a.n_tiles = d.d_model / T_BN;
   if ((e = run_gemm<T, BWD_DX>(a, round8(mtb * a.n_tiles), s, "gemm_bwd_dx")) != hipSuccess) return e;
   return hipGetLastError();
-}
-
-hipError_t launch_ffn_fwd(const moe_desc& d, const void* x, const void* xp, const int32_t* offsets, const void* wg,
-                          const void* wu, const void* wd, void* yp, void* saved, void* ws, hipStream_t s) {
-  if (d.dtype == MOE_BF16) return ffn_fwd_t<bf16>(d, x, xp, offsets, wg, wu, wd, yp, saved, ws, s);
-  return ffn_fwd_t<float>(d, x, xp, offsets, wg, wu, wd, yp, saved, ws, s);
-}
-
-hipError_t launch_ffn_bwd(const moe_desc& d, const void* x, const void* xp, const void* dy, const void* dyp,
-                          const int32_t* offsets, const void* wg, const void* wu, const void* wd, const void* saved,
-                          void* dxp, void* dwg, void* dwu, void* dwd, void* ws, hipStream_t s) {
-  if (d.dtype == MOE_BF16)
-    return ffn_bwd_t<bf16>(d, x, xp, dy, dyp, offsets, wg, wu, wd, saved, dxp, dwg, dwu, dwd, ws, s);
-  return ffn_bwd_t<float>(d, x, xp, dy, dyp, offsets, wg, wu, wd, saved, dxp, dwg, dwu, dwd, ws, s);
 }
 
 }  // namespace pcmoe
