@@ -11,6 +11,8 @@
  *
  * Conventions shared by every call
  *   - Every tensor pointer is a DEVICE pointer owned by the caller; the library never frees it.
+ *     Tensor pointers must be 16-byte aligned and workspace pointers 256-byte aligned (as any
+ *     hipMalloc / torch allocation is); logit_bias only needs 4-byte alignment.
  *   - Every call only validates its arguments and enqueues kernels on `stream`; it never
  *     allocates, frees or synchronises. Results are ready when the stream reaches them.
  *   - Row-major layouts. Weights are [out, in] (so every contraction reads K contiguously from
@@ -24,8 +26,8 @@
  *   - Per-expert counts never travel to the host: grouped kernels read `offsets` on device.
  *   - Errors: a non-zero moe_status is returned and nothing is enqueued; arguments are
  *     checked before any launch. moe_last_error() gives a thread-local explanation.
- *     MOE_ERR_INVALID_ARGUMENT: null pointer, k<1, k>E, bad shard range, bias_groups not
- *       dividing T, bad dtype. MOE_ERR_UNSUPPORTED: d_model or d_ff not a multiple of 128,
+ *     MOE_ERR_INVALID_ARGUMENT: null or misaligned pointer, k<1, k>E, bad shard range,
+ *       bias_groups not dividing T, bad dtype. MOE_ERR_UNSUPPORTED: d_model or d_ff not a multiple of 128,
  *       E > 256, k > 8, T*k*d beyond int32 row indexing. MOE_ERR_WORKSPACE_TOO_SMALL: ws_bytes
  *       below moe_workspace_size(). MOE_ERR_HIP: a kernel launch failed.
  *   - Calls are reentrant; concurrent calls must use distinct output and workspace buffers.

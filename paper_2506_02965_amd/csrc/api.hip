@@ -62,9 +62,11 @@ moe_status check_desc(const moe_desc* d) {
   return MOE_OK;
 }
 
-#define NEED(p)                                                   \
-  do {                                                            \
-    if (!(p)) return fail(MOE_ERR_INVALID_ARGUMENT, #p " is NULL"); \
+// Every buffer is read and written in 16-byte vectors.
+#define NEED(p)                                                                         \
+  do {                                                                                  \
+    if (!(p)) return fail(MOE_ERR_INVALID_ARGUMENT, #p " is NULL");                     \
+    if ((uintptr_t)(p) & 15) return fail(MOE_ERR_INVALID_ARGUMENT, #p " is not 16-byte aligned"); \
   } while (0)
 
 #define NEED_WS(have, need)                                                                                   \
@@ -73,6 +75,7 @@ moe_status check_desc(const moe_desc* d) {
     if ((have) < need_)                                                                                       \
       return fail(MOE_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes, %zu needed", (size_t)(have), need_); \
     if (need_ && !ws) return fail(MOE_ERR_INVALID_ARGUMENT, "ws is NULL");                                    \
+    if ((uintptr_t)ws & 255) return fail(MOE_ERR_INVALID_ARGUMENT, "ws is not 256-byte aligned");             \
   } while (0)
 
 // ------------------------------------------------------------------ per-kernel timing
@@ -150,6 +153,7 @@ moe_status moe_route(const moe_desc* d, const void* x, const void* w_router, con
   moe_status st = check_desc(d);
   if (st) return st;
   NEED(x); NEED(w_router); NEED(logits); NEED(topk_idx); NEED(topk_w);
+  if (logit_bias && ((uintptr_t)logit_bias & 3)) return fail(MOE_ERR_INVALID_ARGUMENT, "logit_bias misaligned");
   if (logit_bias && (bias_groups < 1 || d->T % bias_groups))
     return fail(MOE_ERR_INVALID_ARGUMENT, "bias_groups=%d must divide T=%d", bias_groups, d->T);
   return hip_status(launch_route_fwd(*d, x, w_router, logit_bias, logit_bias ? bias_groups : 1, logits, topk_idx,

@@ -433,7 +433,7 @@ static int tile_shape(int kind, const moe_desc& d) {
   }
   if (table[kind] >= 0) return table[kind];
   (void)d;
-  return T128x128s2;
+  return T256x256w16;
 }
 
 // Upper bound on the m-tiles of the row-ragged kinds (per-expert counts stay on the device).
@@ -488,7 +488,7 @@ static int fit_shape(int sh, int M, int N) {
   if (N % bn) bn = 128;
   if (bm == kShapeBM[sh] && bn == kShapeBN[sh]) return sh;
   const bool k32 = sh == T256x256k32 || sh == T256x128k32 || sh == T128x128k32;
-  if (sh == T256x256w16 && bn == 128) return bm == 256 ? T256x128w8 : T128x128s2;
+  if (sh == T256x256w16) return T128x128s2;  // measured best when one side must drop to 128
   if (bm == 256 && bn == 128) return k32 ? T256x128k32 : T256x128w8;
   if (bm == 128 && bn == 256) return T128x256w8;
   return k32 ? T128x128k32 : T128x128s2;

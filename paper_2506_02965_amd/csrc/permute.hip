@@ -204,6 +204,8 @@ hipError_t launch_permute(const moe_desc& d, const int32_t* idx, const void* x, 
 }
 
 // dx_t = sum_j dx_perm[row(t,j)] + sum_s dx_perm[T*k + s*T + t] (+ sum_e dlogits[t,e] * w_router[e])
+// One wavefront per token. The token's dlogits row is read once; its nonzero experts (k of them when
+// the gate weights are renormalised) are found with ballots and only their router rows are read.
 template <typename T>
 __global__ __launch_bounds__(256) void unpermute_kernel(int Tn, int k, int S, int E, int cpr,
                                                         const Chunk* __restrict__ dxp,
@@ -219,6 +221,16 @@ __global__ __launch_bounds__(256) void unpermute_kernel(int Tn, int k, int S, in
     int rows[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) rows[j] = (j < k) ? s2r[(size_t)t * k + j] : -1;
+    float g[4] = {0.f, 0.f, 0.f, 0.f};
+    uint64_t nz[4] = {0ull, 0ull, 0ull, 0ull};
+    if (dl) {
+#pragma unroll
+      for (int qq = 0; qq < 4; ++qq) {
+        const int e = lane + 64 * qq;
+        g[qq] = (e < E) ? dl[(size_t)t * E + e] : 0.f;
+        nz[qq] = __ballot(g[qq] != 0.f);
+      }
+    }
     for (int c = lane; c < cpr; c += 64) {
       float acc[N];
 #pragma unroll
@@ -237,14 +249,16 @@ __global__ __launch_bounds__(256) void unpermute_kernel(int Tn, int k, int S, in
 #pragma unroll
         for (int i = 0; i < N; ++i) acc[i] += v[i];
       }
-      if (dl) {
-        for (int e = 0; e < E; ++e) {
-          const float g = dl[(size_t)t * E + e];
-          if (g != 0.f) {
-            chunk_to_f<T>(wr[(size_t)e * cpr + c], v);
 #pragma unroll
-            for (int i = 0; i < N; ++i) acc[i] = fmaf(g, v[i], acc[i]);
-          }
+      for (int qq = 0; qq < 4; ++qq) {
+        uint64_t m = nz[qq];
+        while (m) {  // wave-uniform loop over the nonzero experts, in increasing order
+          const int e = __builtin_ctzll(m) + 64 * qq;
+          m &= m - 1;
+          const float ge = dl[(size_t)t * E + e];  // same address in every lane (lanes past cpr are idle here)
+          chunk_to_f<T>(wr[(size_t)e * cpr + c], v);
+#pragma unroll
+          for (int i = 0; i < N; ++i) acc[i] = fmaf(ge, v[i], acc[i]);
         }
       }
       dx[(size_t)t * cpr + c] = f_to_chunk<T>(acc);

@@ -1,94 +1,93 @@
 // Gating (Alg. 7: scores, softmax, TopKIndices, w = p[I]) and its adjoint on the data owner.
 //
-// Scores are accumulated in fp64 from the exact products of the stored inputs and rounded once
-// to fp32, so the top-k decision is reproducible from the inputs alone. Selection happens at
+// Scores are accumulated in fp64 (MFMA f64) from the exact products of the stored inputs and rounded
+// once to fp32, so the top-k decision is reproducible from the inputs alone. Selection happens at
 // wavefront level: k rounds of a 64-lane butterfly argmax on (score, -expert index).
 #include "pcmoe_internal.h"
 #include <math.h>
 
 namespace pcmoe {
 
-constexpr int RT_TOK = 64;  // tokens per block
-constexpr int RT_DC = 64;   // d-columns staged in LDS per step
-constexpr int RT_PITCH = RT_DC + 1;
+typedef double doublex4 __attribute__((ext_vector_type(4)));
 
-// NE = experts per thread (16 expert lanes per block): E <= 16*NE.
-template <typename T, int NE>
+constexpr int RT_TOK = 16;  // tokens per workgroup (one MFMA row block)
+
+// Scores of 16 tokens against all E experts on v_mfma_f64_16x16x4f64. The 4 wavefronts split d into
+// quarters; their fp64 partial sums are added in a fixed order, the bias is added in fp64 and the
+// result is rounded once to fp32. Each lane feeds one 16-byte chunk of its token row and of its
+// expert row (8 bf16 / 4 fp32 consecutive k) into 8 / 4 MFMAs: MFMA s takes element s of every
+// lane, so lane group q contributes k = 4*EPC*c + EPC*q + s (the same mapping on both operands).
+// NET = 16-expert tiles per wavefront (E <= 16 * NET).
+template <typename T, int NET>
 __global__ __launch_bounds__(256) void route_fwd_kernel(const T* __restrict__ x, const T* __restrict__ wr,
                                                         const float* __restrict__ bias, int bias_div, int Tn,
                                                         int d, int E, int k, int renorm,
                                                         float* __restrict__ logits, int32_t* __restrict__ idx,
                                                         float* __restrict__ gw) {
-  extern __shared__ float sm[];
-  float* xs = sm;                       // [64][65]
-  float* wsm = sm + RT_TOK * RT_PITCH;  // [E][65]
-  const int tid = threadIdx.x;
+  constexpr int EP = EPC<T>::value;   // elements per 16-byte chunk
+  constexpr int EW = 16 * NET + 1;    // padded expert stride of the partial-sum table
+  extern __shared__ double part[];    // [4 waves][16 tokens][EW]
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i = lane & 15, q = lane >> 4;
   const int t0 = blockIdx.x * RT_TOK;
-  const int tt = tid & 15, te = tid >> 4;
-
-  double acc[4][NE];
+  const int t = t0 + i;
+  const int kq = d / 4;
+  const int kb = wave * kq;
+  doublex4 acc[NET];
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int et = 0; et < NET; ++et) acc[et] = doublex4{0.0, 0.0, 0.0, 0.0};
+  const T* xrow = x + (size_t)(t < Tn ? t : 0) * d;
+  for (int c = kb; c < kb + kq; c += 4 * EP) {
+    float xf[EP];
+    if (t < Tn) chunk_to_f<T>(ld_chunk(xrow + c + EP * q), xf);
+    else {
 #pragma unroll
-    for (int b = 0; b < NE; ++b) acc[a][b] = 0.0;
-
-  for (int k0 = 0; k0 < d; k0 += RT_DC) {
-    __syncthreads();
-    for (int i = tid; i < RT_TOK * RT_DC; i += 256) {
-      int r = i / RT_DC, c = i % RT_DC, t = t0 + r;
-      xs[r * RT_PITCH + c] = (t < Tn) ? to_f(x[(size_t)t * d + k0 + c]) : 0.f;
+      for (int s = 0; s < EP; ++s) xf[s] = 0.f;
     }
-    for (int i = tid; i < E * RT_DC; i += 256) {
-      int r = i / RT_DC, c = i % RT_DC;
-      wsm[r * RT_PITCH + c] = to_f(wr[(size_t)r * d + k0 + c]);
-    }
-    __syncthreads();
-#pragma unroll 4
-    for (int c = 0; c < RT_DC; ++c) {
-      double xv[4];
 #pragma unroll
-      for (int a = 0; a < 4; ++a) xv[a] = (double)xs[(tt + 16 * a) * RT_PITCH + c];
+    for (int et = 0; et < NET; ++et) {
+      const int e = 16 * et + i;
+      float wf[EP];
+      if (e < E) chunk_to_f<T>(ld_chunk(wr + (size_t)e * d + c + EP * q), wf);
+      else {
 #pragma unroll
-      for (int b = 0; b < NE; ++b) {
-        int e = te + 16 * b;
-        double wv = (e < E) ? (double)wsm[e * RT_PITCH + c] : 0.0;
-#pragma unroll
-        for (int a = 0; a < 4; ++a) acc[a][b] = fma(xv[a], wv, acc[a][b]);
+        for (int s = 0; s < EP; ++s) wf[s] = 0.f;
       }
+#pragma unroll
+      for (int s = 0; s < EP; ++s)
+        acc[et] = __builtin_amdgcn_mfma_f64_16x16x4f64((double)xf[s], (double)wf[s], acc[et], 0, 0, 0);
     }
   }
-  __syncthreads();
-  // scores (+ bias) rounded once to fp32; keep the block's tile in LDS for the selection
-  float* lsm = sm;  // [64][E+1]
-  const int lp = E + 1;
+  // f64 16x16x4 output: register r of lane group q holds D[token 4r + q][expert 16 et + i]
 #pragma unroll
-  for (int a = 0; a < 4; ++a) {
-    int r = tt + 16 * a, t = t0 + r;
+  for (int et = 0; et < NET; ++et)
 #pragma unroll
-    for (int b = 0; b < NE; ++b) {
-      int e = te + 16 * b;
-      if (t < Tn && e < E) {
-        double v = acc[a][b];
-        if (bias) v += (double)bias[(size_t)(t / bias_div) * E + e];
-        float L = (float)v;
-        logits[(size_t)t * E + e] = L;
-        lsm[r * lp + e] = L;
-      }
-    }
-  }
+    for (int r = 0; r < 4; ++r) part[(wave * 16 + 4 * r + q) * EW + 16 * et + i] = acc[et][r];
   __syncthreads();
 
-  const int lane = tid & 63, wave = tid >> 6;
-  for (int r = wave; r < RT_TOK; r += 4) {
-    const int t = t0 + r;
-    if (t >= Tn) break;
+  // four tokens per wavefront: fixed-order sum of the quarters, bias, one rounding, then top-k
+  for (int rr = 0; rr < 4; ++rr) {
+    const int row = wave * 4 + rr;
+    const int tt = t0 + row;
+    if (tt >= Tn) break;
     float v[4];
     bool taken[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      int e = lane + 64 * q;
-      v[q] = (e < E) ? lsm[r * lp + e] : -INFINITY;
-      taken[q] = (e >= E);
+    for (int qq = 0; qq < 4; ++qq) {
+      const int e = lane + 64 * qq;
+      v[qq] = -INFINITY;
+      taken[qq] = true;
+      if (e < E) {
+        double sum = part[(0 * 16 + row) * EW + e];
+        sum += part[(1 * 16 + row) * EW + e];
+        sum += part[(2 * 16 + row) * EW + e];
+        sum += part[(3 * 16 + row) * EW + e];
+        if (bias) sum += (double)bias[(size_t)(tt / bias_div) * E + e];
+        const float L = (float)sum;
+        logits[(size_t)tt * E + e] = L;
+        v[qq] = L;
+        taken[qq] = false;
+      }
     }
     float myv = -INFINITY;
     int myi = 0;
@@ -96,45 +95,45 @@ __global__ __launch_bounds__(256) void route_fwd_kernel(const T* __restrict__ x,
       float bv = -INFINITY;
       int bi = 0x7fffffff;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        int e = lane + 64 * q;
-        if (!taken[q] && (v[q] > bv || (v[q] == bv && e < bi))) {
-          bv = v[q];
+      for (int qq = 0; qq < 4; ++qq) {
+        const int e = lane + 64 * qq;
+        if (!taken[qq] && (v[qq] > bv || (v[qq] == bv && e < bi))) {
+          bv = v[qq];
           bi = e;
         }
       }
 #pragma unroll
       for (int off = 32; off > 0; off >>= 1) {
-        float ov = __shfl_xor(bv, off, 64);
-        int oi = __shfl_xor(bi, off, 64);
+        const float ov = __shfl_xor(bv, off, 64);
+        const int oi = __shfl_xor(bi, off, 64);
         if (ov > bv || (ov == bv && oi < bi)) {
           bv = ov;
           bi = oi;
         }
       }
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if (lane + 64 * q == bi) taken[q] = true;
+      for (int qq = 0; qq < 4; ++qq)
+        if (lane + 64 * qq == bi) taken[qq] = true;
       if (lane == j) {
         myv = bv;
         myi = bi;
       }
     }
     const float m = __shfl(myv, 0, 64);  // the largest score of the token
-    float ex = (lane < k) ? expf(myv - m) : 0.f;
+    const float ex = (lane < k) ? expf(myv - m) : 0.f;
     float Z;
     if (renorm) {
       Z = wave_sum(ex);
     } else {
-      float part = 0.f;
+      float pz = 0.f;
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if (lane + 64 * q < E) part += expf(v[q] - m);
-      Z = wave_sum(part);
+      for (int qq = 0; qq < 4; ++qq)
+        if (lane + 64 * qq < E) pz += expf(v[qq] - m);
+      Z = wave_sum(pz);
     }
     if (lane < k) {
-      idx[(size_t)t * k + lane] = myi;
-      gw[(size_t)t * k + lane] = ex / Z;
+      idx[(size_t)tt * k + lane] = myi;
+      gw[(size_t)tt * k + lane] = ex / Z;
     }
   }
 }
@@ -144,23 +143,23 @@ static hipError_t route_fwd_t(const moe_desc& d, const void* x, const void* wr, 
                               float* logits, int32_t* idx, float* w, hipStream_t s) {
   const int E = d.n_experts;
   dim3 grid((d.T + RT_TOK - 1) / RT_TOK);
-  size_t lds_a = (size_t)(RT_TOK + E) * RT_PITCH * sizeof(float);
-  size_t lds_b = (size_t)RT_TOK * (E + 1) * sizeof(float);
-  size_t lds = lds_a > lds_b ? lds_a : lds_b;
-  int div = d.T / (bg > 0 ? bg : 1);
+  const int div = d.T / (bg > 0 ? bg : 1);
   KernelTimer kt("route_fwd", s);
-#define RT_LAUNCH(NE)                                                                                            \
-  do {                                                                                                           \
-    if (lds > 65536) {                                                                                           \
-      hipError_t e_ = hipFuncSetAttribute((const void*)route_fwd_kernel<T, NE>,                                   \
-                                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);                 \
-      if (e_ != hipSuccess) return e_;                                                                           \
-    }                                                                                                            \
-    hipLaunchKernelGGL((route_fwd_kernel<T, NE>), grid, dim3(256), lds, s, (const T*)x, (const T*)wr, bias, div, \
-                       d.T, d.d_model, E, d.top_k, d.renormalize, logits, idx, w);                               \
+#define RT_LAUNCH(NET)                                                                                          \
+  do {                                                                                                          \
+    const size_t lds = (size_t)4 * 16 * (16 * NET + 1) * sizeof(double);                                       \
+    if (lds > 65536) {                                                                                          \
+      hipError_t e_ = hipFuncSetAttribute((const void*)route_fwd_kernel<T, NET>,                                 \
+                                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);                \
+      if (e_ != hipSuccess) return e_;                                                                          \
+    }                                                                                                           \
+    hipLaunchKernelGGL((route_fwd_kernel<T, NET>), grid, dim3(256), lds, s, (const T*)x, (const T*)wr, bias,     \
+                       div, d.T, d.d_model, E, d.top_k, d.renormalize, logits, idx, w);                         \
   } while (0)
   if (E <= 16) RT_LAUNCH(1);
+  else if (E <= 32) RT_LAUNCH(2);
   else if (E <= 64) RT_LAUNCH(4);
+  else if (E <= 128) RT_LAUNCH(8);
   else RT_LAUNCH(16);
 #undef RT_LAUNCH
   return hipGetLastError();
@@ -240,61 +239,79 @@ __global__ __launch_bounds__(256) void route_dlogits_kernel(int Tn, int E, int k
   }
 }
 
-// Partial dW_router over one chunk of tokens: part[chunk][e][c] = sum_{t in chunk} dl[t][e] * x[t][c].
-constexpr int RB_TOK = 64;
-template <typename T, int NE4>
+// Partial dW_router over one chunk of tokens, part[chunk][e][c] = sum_{t in chunk} dl[t][e] * x[t][c], as an
+// fp32 MFMA contraction (v_mfma_f32_16x16x4f32, tokens as K). Wavefront w of a workgroup owns 16
+// columns c0 + 16w .. +15 and every expert (NET tiles of 16); lane (q, i) feeds dl[t + q][16 et + i]
+// and x[t + q][c0 + 16 w + i] for 4 tokens per MFMA, 8 token-steps in flight.
+template <typename T, int NET>
 __global__ __launch_bounds__(256) void route_dw_partial_kernel(int Tn, int d, int E, int tok_per_chunk,
                                                                const T* __restrict__ x,
                                                                const float* __restrict__ dl,
                                                                float* __restrict__ part) {
-  extern __shared__ float dls[];  // [RB_TOK][E]
-  const int tid = threadIdx.x;
-  const int c = blockIdx.x * 64 + (tid & 63);
-  const int er = tid >> 6;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int q = lane >> 4, i = lane & 15;
+  const int c = blockIdx.x * 64 + 16 * wave + i;
   const int chunk = blockIdx.y;
   const int tb = chunk * tok_per_chunk;
   const int te = min(Tn, tb + tok_per_chunk);
-  float acc[NE4];
+  floatx4 acc[NET];
 #pragma unroll
-  for (int b = 0; b < NE4; ++b) acc[b] = 0.f;
-  for (int s0 = tb; s0 < te; s0 += RB_TOK) {
-    const int n = min(RB_TOK, te - s0);
-    __syncthreads();
-    for (int i = tid; i < n * E; i += 256) dls[i] = dl[(size_t)s0 * E + i];
-    __syncthreads();
-    for (int r = 0; r < n; ++r) {
-      float xv = to_f(x[(size_t)(s0 + r) * d + c]);
+  for (int et = 0; et < NET; ++et) acc[et] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int t0 = tb; t0 < te; t0 += 32) {
+    float a[8][NET], b[8];
 #pragma unroll
-      for (int b = 0; b < NE4; ++b) {
-        int e = er + 4 * b;
-        if (e < E) acc[b] = fmaf(dls[r * E + e], xv, acc[b]);
+    for (int u = 0; u < 8; ++u) {
+      const int t = t0 + 4 * u + q;
+      const bool ok = t < te;
+      b[u] = ok ? to_f(x[(size_t)t * d + c]) : 0.f;
+#pragma unroll
+      for (int et = 0; et < NET; ++et) {
+        const int e = 16 * et + i;
+        a[u][et] = (ok && e < E) ? dl[(size_t)t * E + e] : 0.f;
       }
     }
-  }
 #pragma unroll
-  for (int b = 0; b < NE4; ++b) {
-    int e = er + 4 * b;
-    if (e < E) part[((size_t)chunk * E + e) * d + c] = acc[b];
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int et = 0; et < NET; ++et)
+        acc[et] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u][et], b[u], acc[et], 0, 0, 0);
   }
+  // register r of lane group q holds D[expert 16 et + 4q + r][column c]
+#pragma unroll
+  for (int et = 0; et < NET; ++et)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int e = 16 * et + 4 * q + r;
+      if (e < E) part[((size_t)chunk * E + e) * d + c] = acc[et][r];
+    }
 }
 
-__global__ __launch_bounds__(256) void route_dw_reduce_kernel(int n, int nchunks, const float* __restrict__ part,
-                                                              float* __restrict__ out) {
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
-    float s = 0.f;
-    for (int c = 0; c < nchunks; ++c) s += part[(size_t)c * n + i];
+// dW_router[i] = sum over chunks in order of part[chunk][i]; four elements per thread.
+__global__ __launch_bounds__(256) void route_dw_reduce_kernel(int n4, int nchunks, const float4* __restrict__ part,
+                                                              float4* __restrict__ out) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += gridDim.x * blockDim.x) {
+    float4 s = part[i];
+    for (int c = 1; c < nchunks; ++c) {
+      const float4 v = part[(size_t)c * n4 + i];
+      s.x += v.x;
+      s.y += v.y;
+      s.z += v.z;
+      s.w += v.w;
+    }
     out[i] = s;
   }
 }
 
+// Token chunks of the weight-gradient contraction: enough workgroups to fill the chip, chunk sizes a
+// multiple of 32 tokens.
 static void route_bwd_chunks(const moe_desc& d, int* nch, int* tpc) {
-  int ncol = d.d_model / 64;
-  int maxch = (d.T + RB_TOK - 1) / RB_TOK;
+  const int ncol = d.d_model / 64;
+  const int maxch = (d.T + 255) / 256;
   int want = (1024 + ncol - 1) / ncol;
   int n = want < maxch ? want : maxch;
   if (n < 1) n = 1;
   int per = (d.T + n - 1) / n;
-  per = ((per + RB_TOK - 1) / RB_TOK) * RB_TOK;
+  per = ((per + 31) / 32) * 32;
   *tpc = per;
   *nch = (d.T + per - 1) / per;
 }
@@ -323,22 +340,23 @@ static hipError_t route_bwd_t(const moe_desc& d, const void* x, const float* log
   {
     KernelTimer kt("route_dw_partial", s);
     dim3 grid(d.d_model / 64, nch);
-    size_t lds = (size_t)RB_TOK * E * sizeof(float);  // at most 64 KiB (E <= 256)
-#define RB_LAUNCH(NE4)                                                                                        \
-  hipLaunchKernelGGL((route_dw_partial_kernel<T, NE4>), grid, dim3(256), lds, s, d.T, d.d_model, E, tpc, \
+#define RB_LAUNCH(NET)                                                                                           \
+  hipLaunchKernelGGL((route_dw_partial_kernel<T, NET>), grid, dim3(256), 0, s, d.T, d.d_model, E, tpc,           \
                      (const T*)x, dl, part)
-    if (E <= 8) RB_LAUNCH(2);
-    else if (E <= 16) RB_LAUNCH(4);
-    else if (E <= 64) RB_LAUNCH(16);
-    else RB_LAUNCH(64);
+    if (E <= 16) RB_LAUNCH(1);
+    else if (E <= 32) RB_LAUNCH(2);
+    else if (E <= 64) RB_LAUNCH(4);
+    else if (E <= 128) RB_LAUNCH(8);
+    else RB_LAUNCH(16);
 #undef RB_LAUNCH
   }
   {
     KernelTimer kt("route_dw_reduce", s);
-    int n = E * d.d_model;
-    int blocks = (n + 255) / 256;
+    const int n4 = E * d.d_model / 4;
+    int blocks = (n4 + 255) / 256;
     if (blocks > 2048) blocks = 2048;
-    hipLaunchKernelGGL(route_dw_reduce_kernel, dim3(blocks), dim3(256), 0, s, n, nch, part, dwr);
+    hipLaunchKernelGGL(route_dw_reduce_kernel, dim3(blocks), dim3(256), 0, s, n4, nch, (const float4*)part,
+                       (float4*)dwr);
   }
   return hipGetLastError();
 }
