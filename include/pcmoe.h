@@ -192,6 +192,8 @@ moe_status moe_permute_bwd(const moe_desc* desc, const void* dx_perm, const int3
 /* Per-kernel timing with HIP events recorded around every kernel launch on its own stream
  * (measurement aid; off by default). enable=1 clears the totals and starts recording. */
 moe_status moe_kernel_timing(int enable);
+/* Restricts recording to the launches of one kernel (e.g. "gemm_bwd_dx"); NULL records all. */
+moe_status moe_kernel_timing_select(const char* kernel_name);
 /* Waits for the recorded events and writes "name count total_ms\n" lines into buf. Returns
  * the number of bytes needed (including the terminating NUL). */
 size_t moe_kernel_timing_report(char* buf, size_t buf_bytes);

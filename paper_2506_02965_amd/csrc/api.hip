@@ -82,6 +82,7 @@ moe_status check_desc(const moe_desc* d) {
 struct TimingState {
   std::mutex mu;
   bool on = false;
+  std::string only;  // record only launches with this name (empty: all)
   struct Rec {
     std::string name;
     hipEvent_t a, b;
@@ -101,6 +102,7 @@ KernelTimer::KernelTimer(const char* n, hipStream_t s) : name(n), stream(s), slo
   TimingState& ts = timing();
   std::lock_guard<std::mutex> lk(ts.mu);
   if (!ts.on) return;
+  if (!ts.only.empty() && ts.only != n) return;
   hipEvent_t a = nullptr, b = nullptr;
   if (ts.pool.size() >= 2) {
     a = ts.pool.back(); ts.pool.pop_back();
@@ -252,6 +254,13 @@ moe_status moe_kernel_timing(int enable) {
   }
   ts.recs.clear();
   ts.on = enable != 0;
+  return MOE_OK;
+}
+
+moe_status moe_kernel_timing_select(const char* kernel_name) {
+  TimingState& ts = timing();
+  std::lock_guard<std::mutex> lk(ts.mu);
+  ts.only = kernel_name ? kernel_name : "";
   return MOE_OK;
 }
 

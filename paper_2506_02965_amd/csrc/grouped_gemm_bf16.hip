@@ -388,11 +388,12 @@ static hipError_t run2(const GemmArgs& a, long tiles, hipStream_t s, const char*
 // per SIMD are what keep the MFMA pipes busy: 4-wave 128x128 tiles run two workgroups per CU,
 // the larger tiles use 8 wavefronts in one workgroup.
 enum TileShape { T128x128s2 = 0, T256x128w8, T128x256w8, T256x256w8, T256x256k32, T256x128k32, T128x128k32,
-                 T256x256w16, N_SHAPES };
-static const int kShapeBM[N_SHAPES] = {128, 256, 128, 256, 256, 256, 128, 256};
-static const int kShapeBN[N_SHAPES] = {128, 128, 256, 256, 256, 128, 128, 256};
+                 T256x256w16, T256x256w16k32s4, T256x256w16k32s3, N_SHAPES };
+static const int kShapeBM[N_SHAPES] = {128, 256, 128, 256, 256, 256, 128, 256, 256, 256};
+static const int kShapeBN[N_SHAPES] = {128, 128, 256, 256, 256, 128, 128, 256, 256, 256};
 static const char* kShapeName[N_SHAPES] = {"128x128s2", "256x128w8", "128x256w8", "256x256w8", "256x256k32",
-                                           "256x128k32", "128x128k32", "256x256w16"};
+                                           "256x128k32", "128x128k32", "256x256w16", "256x256w16k32s4",
+                                           "256x256w16k32s3"};
 
 static const char* kKindName[6] = {"gemm_fwd_gate_up", "gemm_fwd_down", "gemm_bwd_dh", "gemm_bwd_dx",
                                    "gemm_wgrad_down", "gemm_wgrad_gate_up"};
@@ -407,6 +408,8 @@ static hipError_t run_shape(int shape, const GemmArgs& a, long tiles, hipStream_
     case T256x128k32: return run2<256, 128, 32, KIND, 4, 4, 2>(a, tiles, s, kKindName[KIND]);
     case T128x128k32: return run2<128, 128, 32, KIND, 3, 2, 2>(a, tiles, s, kKindName[KIND]);
     case T256x256w16: return run2<256, 256, 64, KIND, 2, 4, 4>(a, tiles, s, kKindName[KIND]);
+    case T256x256w16k32s4: return run2<256, 256, 32, KIND, 4, 4, 4>(a, tiles, s, kKindName[KIND]);
+    case T256x256w16k32s3: return run2<256, 256, 32, KIND, 3, 4, 4>(a, tiles, s, kKindName[KIND]);
     default: return run2<256, 256, 64, KIND, 2, 2, 4>(a, tiles, s, kKindName[KIND]);
   }
 }
@@ -488,7 +491,8 @@ static int fit_shape(int sh, int M, int N) {
   if (N % bn) bn = 128;
   if (bm == kShapeBM[sh] && bn == kShapeBN[sh]) return sh;
   const bool k32 = sh == T256x256k32 || sh == T256x128k32 || sh == T128x128k32;
-  if (sh == T256x256w16) return T128x128s2;  // measured best when one side must drop to 128
+  if (sh == T256x256w16 || sh == T256x256w16k32s4 || sh == T256x256w16k32s3)
+    return T128x128s2;  // measured best when one side must drop to 128
   if (bm == 256 && bn == 128) return k32 ? T256x128k32 : T256x128w8;
   if (bm == 128 && bn == 256) return T128x256w8;
   return k32 ? T128x128k32 : T128x128s2;

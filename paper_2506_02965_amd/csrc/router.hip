@@ -306,8 +306,8 @@ __global__ __launch_bounds__(256) void route_dw_reduce_kernel(int n4, int nchunk
 // multiple of 32 tokens.
 static void route_bwd_chunks(const moe_desc& d, int* nch, int* tpc) {
   const int ncol = d.d_model / 64;
-  const int maxch = (d.T + 255) / 256;
-  int want = (1024 + ncol - 1) / ncol;
+  const int maxch = (d.T + 63) / 64;
+  int want = (2048 + ncol - 1) / ncol;
   int n = want < maxch ? want : maxch;
   if (n < 1) n = 1;
   int per = (d.T + n - 1) / n;

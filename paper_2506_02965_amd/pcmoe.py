@@ -20,7 +20,7 @@ MOE_WS_PERMUTE, MOE_WS_FFN_SAVED, MOE_WS_FFN_FWD, MOE_WS_FFN_BWD, MOE_WS_ROUTE_B
 # every symbol include/pcmoe.h declares
 EXPORTS = ("moe_workspace_size", "moe_route", "moe_permute", "moe_expert_ffn_fwd", "moe_combine", "moe_combine_bwd",
            "moe_expert_ffn_bwd", "moe_route_bwd", "moe_permute_bwd", "moe_kernel_timing",
-           "moe_kernel_timing_report", "moe_status_string", "moe_last_error")
+           "moe_kernel_timing_select", "moe_kernel_timing_report", "moe_status_string", "moe_last_error")
 
 
 class moe_desc(ctypes.Structure):
@@ -59,6 +59,7 @@ def lib():
             "moe_route_bwd": (_INT, [D, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
             "moe_permute_bwd": (_INT, [D, _VP, _VP, _VP, _VP, _VP, _VP]),
             "moe_kernel_timing": (_INT, [_INT]),
+            "moe_kernel_timing_select": (_INT, [ctypes.c_char_p]),
             "moe_kernel_timing_report": (_SZ, [ctypes.c_char_p, _SZ]),
             "moe_status_string": (ctypes.c_char_p, [_INT]),
             "moe_last_error": (ctypes.c_char_p, []),
@@ -157,6 +158,11 @@ def moe_permute_bwd(desc, dx_perm, slot_to_row, dlogits, w_router, dx, stream=No
 
 def moe_kernel_timing(enable: bool):
     _check("moe_kernel_timing", lib().moe_kernel_timing(int(bool(enable))))
+
+
+def moe_kernel_timing_select(name: Optional[str]):
+    """Record only the launches of kernel `name` (None: all kernels)."""
+    _check("moe_kernel_timing_select", lib().moe_kernel_timing_select(None if name is None else name.encode()))
 
 
 def moe_kernel_timing_report() -> dict:

@@ -22,7 +22,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 13, names
+    assert len(names) == 14, names
     assert sorted(P.EXPORTS) == names
     L = P.lib()
     for n in names:
@@ -95,4 +95,6 @@ def test_null_pointers_and_workspace():
 
 def test_timing_report_empty():
     P.moe_kernel_timing(False)
+    P.moe_kernel_timing_select("gemm_bwd_dx")
+    P.moe_kernel_timing_select(None)
     assert P.moe_kernel_timing_report() == {}
