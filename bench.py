@@ -32,6 +32,8 @@ HBM_PEAK_GBS = 8000.0
 GEMM_FLOPS_PER_ROW_DF = {
     "gemm_fwd_gate_up": 4.0, "gemm_fwd_down": 2.0, "gemm_bwd_dh": 2.0, "gemm_wgrad_down": 2.0,
     "gemm_wgrad_gate_up": 4.0, "gemm_bwd_dx": 4.0,
+    # two independent contractions in one launch
+    "gemm_bwd_dh+wgrad_down": 4.0, "gemm_bwd_dx+wgrad_gate_up": 8.0,
 }
 
 

@@ -53,7 +53,7 @@ struct TileIdx {
   int g, mt, nt;
 };
 template <bool RAGGED>
-__device__ __forceinline__ bool decode_tile(const GemmArgs& p, TileIdx& t) {
+__device__ __forceinline__ bool decode_tile(const GemmArgs& p, int bid, TileIdx& t) {
   const int G = p.Eloc + p.S;
   int total;
   if (RAGGED) total = p.mt_prefix[G] * p.n_tiles;
@@ -61,7 +61,6 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs& p, TileIdx& t) {
   // Ragged kinds: equal-cost tiles, so each XCD takes a contiguous run of them (its L2 then holds the
   // weights of few groups). Weight-gradient tiles cost K = rows of their group, heaviest groups
   // first; they are dealt round-robin over the XCDs so that the long ones spread out.
-  const int bid = blockIdx.x;
   int L;
   if (RAGGED) {
     const int per_xcd = (total + 7) >> 3;

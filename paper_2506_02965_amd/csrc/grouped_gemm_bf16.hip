@@ -117,18 +117,18 @@ struct Cfg2 {
   static_assert(IA * 1024 * NW == BM * ROWB && IB * 1024 * NW == BN * ROWB, "tiles must split evenly over waves");
 };
 
+// One output tile of contraction KIND: workgroup `bid` of that contraction's tile grid.
 template <int BM, int BN, int BK, int KIND, int STAGES, int WM, int WN>
-__global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs p) {
+__device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem) {
   using C = Cfg2<BM, BN, BK, STAGES, WM, WN>;
   using KT = KindTraits<KIND>;
   constexpr int ES = 2;
-  extern __shared__ __align__(16) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (LDS DMA bases, resources)
   const int wm = wave / WN, wn = wave % WN;
 
   TileIdx ti;
-  if (!decode_tile<KT::ragged_m>(p, ti)) return;
+  if (!decode_tile<KT::ragged_m>(p, bid, ti)) return;
   const int g = ti.g;
   const int d = p.d, f = p.f;
   const bool routed = g < p.Eloc;
@@ -364,6 +364,23 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs p) {
   }
 }
 
+template <int BM, int BN, int BK, int KIND, int STAGES, int WM, int WN>
+__global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs p) {
+  extern __shared__ __align__(16) char smem[];
+  gemm_tile<BM, BN, BK, KIND, STAGES, WM, WN>(p, blockIdx.x, smem);
+}
+
+// Two independent contractions in one launch: workgroups [0, grid_a) take tiles of KA (the longer
+// K loops, so they start first), the rest tiles of KB. The CUs that KA's tile grid leaves idle
+// work through KB meanwhile, instead of idling until the next launch.
+template <int BM, int BN, int BK, int KA, int KB, int STAGES, int WM, int WN>
+__global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_pair_kernel(GemmArgs pa, GemmArgs pb, int grid_a) {
+  extern __shared__ __align__(16) char smem[];
+  const int bid = blockIdx.x;
+  if (bid < grid_a) gemm_tile<BM, BN, BK, KA, STAGES, WM, WN>(pa, bid, smem);
+  else gemm_tile<BM, BN, BK, KB, STAGES, WM, WN>(pb, bid - grid_a, smem);
+}
+
 // ------------------------------------------------------------------------- host side
 
 template <int BM, int BN, int BK, int KIND, int STAGES, int WM, int WN>
@@ -397,6 +414,27 @@ static const char* kShapeName[N_SHAPES] = {"128x128s2", "256x128w8", "128x256w8"
 
 static const char* kKindName[6] = {"gemm_fwd_gate_up", "gemm_fwd_down", "gemm_bwd_dh", "gemm_bwd_dx",
                                    "gemm_wgrad_down", "gemm_wgrad_gate_up"};
+
+template <int BM, int BN, int BK, int KA, int KB, int STAGES, int WM, int WN>
+static hipError_t run_pair2(const GemmArgs& a, long tiles_a, const GemmArgs& b, long tiles_b, hipStream_t s,
+                            const char* name) {
+  using C = Cfg2<BM, BN, BK, STAGES, WM, WN>;
+  static_assert(C::LDS <= 160 * 1024, "LDS budget of one CU");
+  auto kern = gemm_bf16_pair_kernel<BM, BN, BK, KA, KB, STAGES, WM, WN>;
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  // grid_a a multiple of 8 keeps each workgroup of the second contraction on the XCD its index implies
+  const int grid_a = (int)((tiles_a + 7) / 8 * 8);
+  const int grid = grid_a + (int)tiles_b;
+  if (grid <= 0) return hipSuccess;
+  KernelTimer kt(name, s);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(C::NT), C::LDS, s, a, b, grid_a);
+  return hipGetLastError();
+}
 
 template <int KIND>
 static hipError_t run_shape(int shape, const GemmArgs& a, long tiles, hipStream_t s) {
@@ -498,22 +536,60 @@ static int fit_shape(int sh, int M, int N) {
   return k32 ? T128x128k32 : T128x128s2;
 }
 
+// A contraction ready to launch: tile shape, arguments and the workgroups its grid needs.
+struct Prep {
+  int sh;
+  GemmArgs a;
+  long tiles;
+};
+
+// Ragged-M contraction with n_cols output columns in the tile grid (FWD_GU: gate and up columns).
 template <int KIND>
-static hipError_t ragged(const moe_desc& d, GemmArgs a, const Plan& pl, int n_cols, hipStream_t s) {
+static Prep prep_ragged(const moe_desc& d, GemmArgs a, const Plan& pl, int n_cols) {
   const int sh = fit_shape(tile_shape(KIND, d), 0, n_cols);
   const int bm = kShapeBM[sh], bn = kShapeBN[sh];
   a.mt_prefix = bm == 128 ? pl.pre128 : pl.pre256;
   a.n_tiles = n_cols / bn;  // FWD_GU: n_cols = 2f, each tile holds bn/2 gate and bn/2 up columns
-  return run_shape<KIND>(sh, a, mtile_bound2(d, bm) * a.n_tiles, s);
+  return Prep{sh, a, mtile_bound2(d, bm) * a.n_tiles};
 }
-
+// Weight gradient: an M x N output per group, K = the group's rows.
 template <int KIND>
-static hipError_t wgrad(const moe_desc& d, GemmArgs a, const Plan& pl, int M, int N, hipStream_t s) {
+static Prep prep_wgrad(const moe_desc& d, GemmArgs a, const Plan& pl, int M, int N) {
   const int sh = fit_shape(tile_shape(KIND, d), M, N);
   a.order = pl.order;
   a.m_tiles = M / kShapeBM[sh];
   a.n_tiles = N / kShapeBN[sh];
-  return run_shape<KIND>(sh, a, (long)(d.local_count + d.n_shared) * a.m_tiles * a.n_tiles, s);
+  return Prep{sh, a, (long)(d.local_count + d.n_shared) * a.m_tiles * a.n_tiles};
+}
+template <int KIND>
+static hipError_t run(const Prep& p, hipStream_t s) {
+  return run_shape<KIND>(p.sh, p.a, p.tiles, s);
+}
+
+// PCMOE_PAIR=0 launches the paired contractions one after the other instead.
+static bool pair_enabled() {
+  static int on = -1;
+  if (on < 0) {
+    const char* env = getenv("PCMOE_PAIR");
+    on = !(env && env[0] == '0');
+  }
+  return on;
+}
+
+// Independent contractions A and B (no operand of one is written by the other) in one launch when
+// they share a tile shape; A's workgroups come first.
+template <int KA, int KB>
+static hipError_t run_pair(const Prep& A, const Prep& B, hipStream_t s, const char* name) {
+  if (A.sh == B.sh && pair_enabled()) {
+    switch (A.sh) {
+      case T256x256w16: return run_pair2<256, 256, 64, KA, KB, 2, 4, 4>(A.a, A.tiles, B.a, B.tiles, s, name);
+      case T128x128s2: return run_pair2<128, 128, 64, KA, KB, 2, 2, 2>(A.a, A.tiles, B.a, B.tiles, s, name);
+      default: break;
+    }
+  }
+  hipError_t e = run<KA>(A, s);
+  if (e != hipSuccess) return e;
+  return run<KB>(B, s);
 }
 
 hipError_t launch_ffn_fwd(const moe_desc& d, const void* x, const void* xp, const int32_t* offsets, const void* wg,
@@ -527,9 +603,8 @@ hipError_t launch_ffn_fwd(const moe_desc& d, const void* x, const void* xp, cons
   a.h = (char*)saved + align256(R * 2 * d.d_ff * 2);
   a.out = yp;
   hipError_t e;
-  if ((e = ragged<FWD_GU>(d, a, pl, 2 * d.d_ff, s)) != hipSuccess) return e;
-  if ((e = ragged<FWD_DOWN>(d, a, pl, d.d_model, s)) != hipSuccess) return e;
-  return hipGetLastError();
+  if ((e = run<FWD_GU>(prep_ragged<FWD_GU>(d, a, pl, 2 * d.d_ff), s)) != hipSuccess) return e;
+  return run<FWD_DOWN>(prep_ragged<FWD_DOWN>(d, a, pl, d.d_model), s);
 }
 
 hipError_t launch_ffn_bwd(const moe_desc& d, const void* x, const void* xp, const void* dy, const void* dyp,
@@ -545,16 +620,20 @@ hipError_t launch_ffn_bwd(const moe_desc& d, const void* x, const void* xp, cons
   a.gu = (void*)saved;
   a.h = (char*)saved + align256(R * 2 * d.d_ff * 2);
   a.dgu = dgu;
-  hipError_t e;
-  if ((e = ragged<BWD_DH>(d, a, pl, d.d_ff, s)) != hipSuccess) return e;
-  a.out = dwd;
-  if ((e = wgrad<WG_DOWN>(d, a, pl, d.d_model, d.d_ff, s)) != hipSuccess) return e;
-  a.out = dwg;
-  a.out2 = dwu;
-  if ((e = wgrad<WG_GU>(d, a, pl, 2 * d.d_ff, d.d_model, s)) != hipSuccess) return e;
-  a.out = dxp;
-  if ((e = ragged<BWD_DX>(d, a, pl, d.d_model, s)) != hipSuccess) return e;
-  return hipGetLastError();
+  // dG|dU (BWD_DH) and dW_down (WG_DOWN) read only forward results and dY; dX (BWD_DX) and
+  // dW_gate|dW_up (WG_GU) both read dG|dU.
+  GemmArgs a_wd = a, a_wgu = a, a_dx = a;
+  a_wd.out = dwd;
+  a_wgu.out = dwg;
+  a_wgu.out2 = dwu;
+  a_dx.out = dxp;
+  hipError_t e = run_pair<BWD_DH, WG_DOWN>(prep_ragged<BWD_DH>(d, a, pl, d.d_ff),
+                                           prep_wgrad<WG_DOWN>(d, a_wd, pl, d.d_model, d.d_ff), s,
+                                           "gemm_bwd_dh+wgrad_down");
+  if (e != hipSuccess) return e;
+  return run_pair<BWD_DX, WG_GU>(prep_ragged<BWD_DX>(d, a_dx, pl, d.d_model),
+                                 prep_wgrad<WG_GU>(d, a_wgu, pl, 2 * d.d_ff, d.d_model), s,
+                                 "gemm_bwd_dx+wgrad_gate_up");
 }
 
 }  // namespace pcmoe

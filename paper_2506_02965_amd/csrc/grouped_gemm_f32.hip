@@ -139,7 +139,7 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(GemmArgs p) 
 
   // ---------------------------------------------------------------- tile decode
   TileIdx ti;
-  if (!decode_tile<KT::ragged_m>(p, ti)) return;
+  if (!decode_tile<KT::ragged_m>(p, blockIdx.x, ti)) return;
   const int g = ti.g, mt = ti.mt, nt = ti.nt;
 
   const bool routed = g < p.Eloc;
