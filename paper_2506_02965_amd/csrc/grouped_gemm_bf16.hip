@@ -22,10 +22,6 @@ namespace pcmoe {
 typedef int int32x4 __attribute__((ext_vector_type(4)));
 typedef short short4v __attribute__((ext_vector_type(4)));
 
-extern "C" __device__ void llvm_amdgcn_raw_buffer_load_lds(int32x4 rsrc, __attribute__((address_space(3))) uint32_t* lds,
-                                                           int size, int voffset, int soffset, int offset, int aux)
-    __asm("llvm.amdgcn.raw.buffer.load.lds");
-
 // Buffer resource over [base, base + bytes): loads at offsets >= bytes return zeros.
 __device__ __forceinline__ int32x4 make_rsrc(const void* base, uint32_t bytes) {
   struct {
@@ -41,8 +37,22 @@ __device__ __forceinline__ int32x4 make_rsrc(const void* base, uint32_t bytes) {
   return v;
 }
 
-__device__ __forceinline__ void dma16(int32x4 rsrc, char* lds_dst, int voff) {
-  llvm_amdgcn_raw_buffer_load_lds(rsrc, (__attribute__((address_space(3))) uint32_t*)lds_dst, 16, voff, 0, 0, 0);
+// 16 bytes per lane from the buffer at byte offset voff into LDS at lds_dst + 16 * lane. Written as
+// inline assembly on purpose: through the builtin, the compiler sees an LDS store it cannot tell apart
+// from the operand buffer being read, and waits for every outstanding load (vmcnt(0)) before the next
+// LDS read, which serialises each K-tile's load latency with the previous tile's MFMAs. Completion is
+// tracked by the explicit vmcnt waits of the main loop instead.
+__device__ __forceinline__ uint32_t lds_addr(const char* p) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p);
+}
+__device__ __forceinline__ void dma16(int32x4 rsrc, uint32_t m0, int voff) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %1, %2, 0 offen lds"
+      :
+      : "s"(m0), "v"(voff), "s"(rsrc)
+      : "memory", "m0");
 }
 
 // K-contiguous tile rows of BK bf16 (BK = 64: 8 chunks of 16 bytes; BK = 32: 4 chunks): chunk c of row r
@@ -221,20 +231,21 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
   }
 
   // Direct load number idx (0 .. LOADS-1) of K-tile kt into LDS stage `stage`.
+  const uint32_t lds0 = lds_addr(smem) + wave * 1024;
   auto issue_one = [&](int kt, int stage, int idx) {
-    char* As = smem + stage * C::STAGE_BYTES;
-    char* Bs = As + BM * C::ROWB;
+    const uint32_t As = lds0 + stage * C::STAGE_BYTES;
+    const uint32_t Bs = As + BM * C::ROWB;
     const int k0 = kt * BK;
     if (idx < C::IA) {
       const int j = idx;
-      dma16(ra, As + (wave + C::NW * j) * 1024, va[j] + (KT::a_kc ? k0 * ES : k0 * a_ld));
+      dma16(ra, As + C::NW * j * 1024, va[j] + (KT::a_kc ? k0 * ES : k0 * a_ld));
     } else {
       const int j = idx - C::IA;
       if (KIND == BWD_DX) {
         const bool up = k0 >= f;
-        dma16(up ? rb1 : rb0, Bs + (wave + C::NW * j) * 1024, vb[j] + (up ? k0 - f : k0) * b_ld);
+        dma16(up ? rb1 : rb0, Bs + C::NW * j * 1024, vb[j] + (up ? k0 - f : k0) * b_ld);
       } else {
-        dma16(bup[j] ? rb1 : rb0, Bs + (wave + C::NW * j) * 1024, vb[j] + (KT::b_kc ? k0 * ES : k0 * b_ld));
+        dma16(bup[j] ? rb1 : rb0, Bs + C::NW * j * 1024, vb[j] + (KT::b_kc ? k0 * ES : k0 * b_ld));
       }
     }
   };
@@ -260,7 +271,8 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
     // tile kt has landed when at most the later tiles' loads are outstanding
     if (kt + STAGES - 2 < KTN) wait_vmcnt<(STAGES - 2) * C::LOADS>();
     else wait_vmcnt<0>();
-    __syncthreads();
+    // every wave's loads of tile kt have landed and its reads of the stage about to be refilled are done
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     if (kt + STAGES - 1 < KTN) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
     const char* As = smem + (kt % STAGES) * C::STAGE_BYTES;
     const char* Bs = As + BM * C::ROWB;
