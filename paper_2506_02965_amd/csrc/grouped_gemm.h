@@ -37,26 +37,47 @@ template <> struct KindTraits<WG_GU> { static constexpr bool ragged_m = false, a
 
 constexpr int GROUP_M = 8;  // m-tiles visited together for L2 reuse of the weight tiles
 
-__device__ __forceinline__ int find_group(const int32_t* __restrict__ pre, int G, int L, int nt) {
-  int lo = 0, hi = G - 1;  // largest g with pre[g]*nt <= L
-  while (lo < hi) {
-    int mid = (lo + hi + 1) >> 1;
-    if (pre[mid] * nt <= L) lo = mid;
-    else hi = mid - 1;
-  }
-  return lo;
+// Entry i (wave-uniform) of a small device array spread over the wavefront: lane l holds entry
+// 64 * s + l in v[s].
+template <int NS>
+__device__ __forceinline__ int wave_pick(const int (&v)[NS], int i) {
+  int r = 0;
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+    if ((i >> 6) == s) r = __builtin_amdgcn_readlane(v[s], i & 63);
+  return __builtin_amdgcn_readfirstlane(r);  // keeps the result in a scalar register
 }
 
 // Decode a workgroup's tile: XCD-aware order (consecutive logical tiles on one XCD), groups by
 // device-side prefix, m-tiles in bunches of GROUP_M per n-tile. Returns false for idle workgroups.
+// Called by every lane of the wavefront.
 struct TileIdx {
   int g, mt, nt;
+  int row0, rows;  // the group's first row in its source and its row count
 };
 template <bool RAGGED>
 __device__ __forceinline__ bool decode_tile(const GemmArgs& p, int bid, TileIdx& t) {
+  constexpr int NS = 8;  // 8 x 64 entries per array: groups <= 511
   const int G = p.Eloc + p.S;
+  const int lane = threadIdx.x & 63;
+  const int ns = (G + 64) >> 6;  // slots covering entries 0..G
+  // One batch of independent loads (a chain of dependent ones costs a memory latency each): the
+  // m-tile prefix (ragged kinds), the group order (weight gradients) and the row offsets.
+  int pre[NS], ord[NS], off[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    const int i = 64 * s + lane;
+    pre[s] = 0;
+    ord[s] = 0;
+    off[s] = 0;
+    if (s < ns) {
+      if (RAGGED && i <= G) pre[s] = p.mt_prefix[i];
+      if (!RAGGED && p.order && i < G) ord[s] = p.order[i];
+      if (i <= p.Eloc) off[s] = p.offsets[i];
+    }
+  }
   int total;
-  if (RAGGED) total = p.mt_prefix[G] * p.n_tiles;
+  if (RAGGED) total = wave_pick(pre, G) * p.n_tiles;
   else total = G * p.m_tiles * p.n_tiles;
   // Ragged kinds: equal-cost tiles, so each XCD takes a contiguous run of them (its L2 then holds the
   // weights of few groups). Weight-gradient tiles cost K = rows of their group, heaviest groups
@@ -72,20 +93,34 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs& p, int bid, TileIdx&
   if (L >= total) return false;
   int l, n_mt;
   if (RAGGED) {
-    t.g = find_group(p.mt_prefix, G, L, p.n_tiles);
-    l = L - p.mt_prefix[t.g] * p.n_tiles;
-    n_mt = p.mt_prefix[t.g + 1] - p.mt_prefix[t.g];
+    // largest g < G with pre[g] * n_tiles <= L (pre is non-decreasing from pre[0] = 0)
+    int g = 0;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      if (s < ns) {
+        const int i = 64 * s + lane;
+        g += __popcll(__ballot(i >= 1 && i < G && pre[s] * p.n_tiles <= L));
+      }
+    }
+    g = __builtin_amdgcn_readfirstlane(g);
+    t.g = g;
+    const int p0 = wave_pick(pre, g);
+    l = L - p0 * p.n_tiles;
+    n_mt = wave_pick(pre, g + 1) - p0;
   } else {
     const int rank = L / (p.m_tiles * p.n_tiles);  // heaviest groups first: their long K loops start early
-    t.g = p.order ? p.order[rank] : rank;
+    t.g = p.order ? wave_pick(ord, rank) : rank;
     l = L - rank * p.m_tiles * p.n_tiles;
     n_mt = p.m_tiles;
   }
+  const bool routed = t.g < p.Eloc;
+  t.row0 = routed ? wave_pick(off, t.g) : 0;
+  t.rows = routed ? wave_pick(off, t.g + 1) - t.row0 : p.T;
   const int mblk = l / (GROUP_M * p.n_tiles);
   const int rem = l - mblk * GROUP_M * p.n_tiles;
   const int gsz = min(GROUP_M, n_mt - mblk * GROUP_M);
-  t.nt = rem / gsz;
-  t.mt = mblk * GROUP_M + rem % gsz;
+  t.nt = __builtin_amdgcn_readfirstlane(rem / gsz);
+  t.mt = __builtin_amdgcn_readfirstlane(mblk * GROUP_M + rem % gsz);
   return true;
 }
 

@@ -142,8 +142,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
   const int g = ti.g;
   const int d = p.d, f = p.f;
   const bool routed = g < p.Eloc;
-  const int row0 = routed ? p.offsets[g] : 0;
-  const int rows = routed ? p.offsets[g + 1] - row0 : p.T;
+  const int row0 = ti.row0, rows = ti.rows;
   const size_t rs = routed ? (size_t)row0 : (size_t)p.rows_cap + (size_t)(g - p.Eloc) * p.T;
   const int m0 = ti.mt * BM, n0 = ti.nt * BN;
   int K;
@@ -326,6 +325,43 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
         for (int r = 0; r < 4; ++r) st[(16 * i + 4 * q + r) * C::PITCH + 16 * j + li] = acc[part * FPP + i][j][r];
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's staging writes are done
     __builtin_amdgcn_wave_barrier();
+    if constexpr (KIND == BWD_DH) {
+      // The SwiGLU adjoint reads the saved G|U of its outputs: the loads of the whole part are issued
+      // together, so their latency is paid once per part rather than once per chunk.
+      constexpr int IT = C::PART_ROWS * CPRW / 64;  // output chunks per lane and part
+      static_assert(IT * 64 == C::PART_ROWS * CPRW, "epilogue chunks per lane");
+      Chunk gch[IT], uch[IT];
+#pragma unroll
+      for (int it = 0; it < IT; ++it) {
+        const int qq = lane + 64 * it, rr = qq / CPRW, cc = (qq % CPRW) * 8;
+        const int m = min(m0 + wm * C::WTM + part * C::PART_ROWS + rr, rows - 1);  // rows past the group: unused
+        const char* gu = (const char*)p.gu + ((rs + m) * 2 * f + n0 + wn * OUT_W + cc) * ES;
+        gch[it] = ld_chunk(gu);
+        uch[it] = ld_chunk(gu + (size_t)f * ES);
+      }
+#pragma unroll
+      for (int it = 0; it < IT; ++it) {
+        const int qq = lane + 64 * it, rr = qq / CPRW, cc = (qq % CPRW) * 8;
+        const int m = m0 + wm * C::WTM + part * C::PART_ROWS + rr;
+        if (m >= rows) continue;
+        float v[8], gv[8], uv[8], dg[8], du[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = st[rr * C::PITCH + cc + e];
+        chunk_to_f<bf16>(gch[it], gv);
+        chunk_to_f<bf16>(uch[it], uv);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float sg = 1.f / (1.f + __expf(-gv[e]));
+          du[e] = v[e] * gv[e] * sg;
+          dg[e] = v[e] * uv[e] * sg * (1.f + gv[e] * (1.f - sg));
+        }
+        char* o = (char*)p.dgu + ((rs + m) * 2 * f + n0 + wn * OUT_W + cc) * ES;
+        st_chunk(o, f_to_chunk<bf16>(dg));
+        st_chunk(o + (size_t)f * ES, f_to_chunk<bf16>(du));
+      }
+      __builtin_amdgcn_wave_barrier();
+      continue;
+    }
     for (int qq = lane; qq < C::PART_ROWS * CPRW; qq += 64) {
       const int rr = qq / CPRW, cc = (qq % CPRW) * 8;
       const int m = m0 + wm * C::WTM + part * C::PART_ROWS + rr;
@@ -348,21 +384,6 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
         st_chunk((char*)p.h + ((rs + m) * f + col) * ES, f_to_chunk<bf16>(hv));
       } else if (KIND == FWD_DOWN || KIND == BWD_DX) {
         st_chunk((char*)p.out + ((rs + m) * d + n0 + wn * OUT_W + cc) * ES, f_to_chunk<bf16>(v));
-      } else if (KIND == BWD_DH) {
-        const int col = n0 + wn * OUT_W + cc;
-        const char* gu = (const char*)p.gu + ((rs + m) * 2 * f + col) * ES;
-        float gv[8], uv[8], dg[8], du[8];
-        chunk_to_f<bf16>(ld_chunk(gu), gv);
-        chunk_to_f<bf16>(ld_chunk(gu + (size_t)f * ES), uv);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float sg = 1.f / (1.f + __expf(-gv[e]));
-          du[e] = v[e] * gv[e] * sg;
-          dg[e] = v[e] * uv[e] * sg * (1.f + gv[e] * (1.f - sg));
-        }
-        char* o = (char*)p.dgu + ((rs + m) * 2 * f + col) * ES;
-        st_chunk(o, f_to_chunk<bf16>(dg));
-        st_chunk(o + (size_t)f * ES, f_to_chunk<bf16>(du));
       } else if (KIND == WG_DOWN) {
         st_chunk((char*)p.out + (((size_t)g * d + m) * f + n0 + wn * OUT_W + cc) * ES, f_to_chunk<bf16>(v));
       } else {  // WG_GU

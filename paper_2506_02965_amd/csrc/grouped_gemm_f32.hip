@@ -143,8 +143,8 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(GemmArgs p) 
   const int g = ti.g, mt = ti.mt, nt = ti.nt;
 
   const bool routed = g < p.Eloc;
-  const int row0 = routed ? p.offsets[g] : 0;                       // first row of the group in its source
-  const int rows = routed ? p.offsets[g + 1] - row0 : p.T;          // rows of the group
+  const int row0 = ti.row0;                                          // first row of the group in its source
+  const int rows = ti.rows;                                          // rows of the group
   const size_t rs = routed ? (size_t)row0 : (size_t)p.rows_cap + (size_t)(g - p.Eloc) * p.T;  // row-space base
   const int d = p.d, f = p.f;
   const size_t es = sizeof(T);
