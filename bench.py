@@ -16,6 +16,7 @@ the host cores.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -35,6 +36,43 @@ GEMM_FLOPS_PER_ROW_DF = {
     # two independent contractions in one launch
     "gemm_bwd_dh+wgrad_down": 4.0, "gemm_bwd_dx+wgrad_gate_up": 8.0,
 }
+
+
+COPY_CAL_BYTES = 256 << 20   # bytes read (and written) by one calibration copy
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_dominant_kernel.txt")
+GEMM_SOURCES = [os.path.join(ROOT, "paper_2506_02965_amd", "csrc", n)
+                for n in ("grouped_gemm_bf16.hip", "grouped_gemm.h", "pcmoe_internal.h")]
+
+
+def gemm_source_digest():
+    h = hashlib.sha256()
+    for path in GEMM_SOURCES:
+        with open(path, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from the FETCH_SIZE / WRITE_SIZE counter passes recorded in
+    TRAFFIC_FILE, each scaled by what the same counter reads for the calibration copy of known size;
+    None when no record matches this kernel, workload and the current GEMM sources."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    rec = {}
+    with open(TRAFFIC_FILE) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                rec[k.strip()] = v.strip()
+    try:
+        if rec["kernel"] != kernel or rec["workload"] != workload or rec["gemm_sources"] != gemm_source_digest():
+            return None
+        cal_kib = COPY_CAL_BYTES / 1024.0
+        fetch = float(rec["fetch_kib_per_launch"]) * cal_kib / float(rec["copy_fetch_kib"])
+        write = float(rec["write_kib_per_launch"]) * cal_kib / float(rec["copy_write_kib"])
+    except (KeyError, ValueError, ZeroDivisionError):
+        return None
+    return round((fetch + write) * 1024.0)
 
 
 def layer_flops(cfg, n_routed_rows, backward=True):
@@ -81,6 +119,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="before the warm-up, copy a 256 MiB device buffer three times (the reference kernel "
+                         "that scales the HBM byte counters of a rocprofv3 --pmc run)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the layer is one party's shard on one MI355X; "
@@ -93,6 +134,13 @@ def main():
     from paper_2506_02965_amd.synth import CONFIGS, make_inputs
 
     P.lib()
+    if args.copy_calibration:
+        src = torch.ones(COPY_CAL_BYTES // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     cfg = CONFIGS[args.config]
     inp = make_inputs(cfg, with_dy=True)
     w = upload(inp, device="cuda")
@@ -140,7 +188,7 @@ def main():
         ach = per_launch / dom_avg_s / 1e12
         peak = BF16_PEAK_TFLOPS if cfg.dtype == "bf16" else FP32_PEAK_TFLOPS
         roof = {"kernel": dom_name, "bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(ach / peak, 4), "traffic": None,
+                "frac": round(ach / peak, 4), "traffic": measured_traffic(dom_name, cfg.name),
                 "algorithmic_per_launch": per_launch, "avg_launch_us": round(dom_avg_s * 1e6, 2)}
     else:
         roof = {"kernel": dom_name, "bound": None, "achieved": None, "peak": None, "unit": None, "frac": None,
