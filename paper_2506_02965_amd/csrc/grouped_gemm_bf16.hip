@@ -51,7 +51,7 @@ __device__ __forceinline__ void dma16(int32x4 rsrc, uint32_t m0, int voff) {
       "s_nop 0\n\t"
       "buffer_load_dwordx4 %1, %2, 0 offen lds"
       :
-      : "s"(m0), "v"(voff), "s"(rsrc)
+      : "s"(__builtin_amdgcn_readfirstlane(m0)), "v"(voff), "s"(rsrc)
       : "memory", "m0");
 }
 

@@ -240,30 +240,44 @@ __global__ __launch_bounds__(256) void route_dlogits_kernel(int Tn, int E, int k
 }
 
 // Partial dW_router over one chunk of tokens, part[chunk][e][c] = sum_{t in chunk} dl[t][e] * x[t][c], as an
-// fp32 MFMA contraction (v_mfma_f32_16x16x4f32, tokens as K). Wavefront w of a workgroup owns 16
-// columns c0 + 16w .. +15 and every expert (NET tiles of 16); lane (q, i) feeds dl[t + q][16 et + i]
-// and x[t + q][c0 + 16 w + i] for 4 tokens per MFMA, 8 token-steps in flight.
-template <typename T, int NET>
+// fp32 MFMA contraction (v_mfma_f32_16x16x4f32, tokens as K). Lane (q, i) of a wavefront loads JJ contiguous
+// columns c0 + JJ*i .. + JJ-1 of token rows t + q (one coalesced load of the row segment per 16 lanes) and
+// feeds column c0 + JJ*i + jj of MFMA number jj; its A operand is dl[t + q][16 et + i]. 8 token-steps of 4
+// tokens are loaded before their MFMAs.
+template <typename T, int JJ>
+struct alignas(JJ * sizeof(T) < 16 ? JJ * sizeof(T) : 16) XRow {  // tensors are 16-byte aligned
+  T v[JJ];
+};
+
+// JJ columns per lane: 8 while the accumulators (JJ x NET tiles) fit, fewer for many experts.
+constexpr int dw_cols_per_lane(int net) { return net <= 2 ? 8 : 16 / net > 0 ? 16 / net : 1; }
+
+template <typename T, int NET, int JJ>
 __global__ __launch_bounds__(256) void route_dw_partial_kernel(int Tn, int d, int E, int tok_per_chunk,
                                                                const T* __restrict__ x,
                                                                const float* __restrict__ dl,
                                                                float* __restrict__ part) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int q = lane >> 4, i = lane & 15;
-  const int c = blockIdx.x * 64 + 16 * wave + i;
+  const int c0 = (blockIdx.x * 4 + wave) * 16 * JJ;  // first column of this wavefront
+  if (c0 >= d) return;                               // d is a multiple of 16 * JJ: all or nothing
   const int chunk = blockIdx.y;
   const int tb = chunk * tok_per_chunk;
   const int te = min(Tn, tb + tok_per_chunk);
-  floatx4 acc[NET];
+  floatx4 acc[JJ][NET];
 #pragma unroll
-  for (int et = 0; et < NET; ++et) acc[et] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int jj = 0; jj < JJ; ++jj)
+#pragma unroll
+    for (int et = 0; et < NET; ++et) acc[jj][et] = floatx4{0.f, 0.f, 0.f, 0.f};
   for (int t0 = tb; t0 < te; t0 += 32) {
-    float a[8][NET], b[8];
+    XRow<T, JJ> xv[8];
+    float a[8][NET];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int t = t0 + 4 * u + q;
       const bool ok = t < te;
-      b[u] = ok ? to_f(x[(size_t)t * d + c]) : 0.f;
+      if (ok) xv[u] = *reinterpret_cast<const XRow<T, JJ>*>(x + (size_t)t * d + c0 + JJ * i);
+      else xv[u] = XRow<T, JJ>{};
 #pragma unroll
       for (int et = 0; et < NET; ++et) {
         const int e = 16 * et + i;
@@ -273,41 +287,67 @@ __global__ __launch_bounds__(256) void route_dw_partial_kernel(int Tn, int d, in
 #pragma unroll
     for (int u = 0; u < 8; ++u)
 #pragma unroll
-      for (int et = 0; et < NET; ++et)
-        acc[et] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u][et], b[u], acc[et], 0, 0, 0);
+      for (int jj = 0; jj < JJ; ++jj) {
+        const float b = to_f(xv[u].v[jj]);
+#pragma unroll
+        for (int et = 0; et < NET; ++et)
+          acc[jj][et] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u][et], b, acc[jj][et], 0, 0, 0);
+      }
   }
-  // register r of lane group q holds D[expert 16 et + 4q + r][column c]
+  // register r of lane group q holds D[expert 16 et + 4q + r][n = i], column c0 + JJ*i + jj
 #pragma unroll
   for (int et = 0; et < NET; ++et)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int e = 16 * et + 4 * q + r;
-      if (e < E) part[((size_t)chunk * E + e) * d + c] = acc[et][r];
+      if (e >= E) continue;
+      float* o = part + ((size_t)chunk * E + e) * d + c0 + JJ * i;
+#pragma unroll
+      for (int jj = 0; jj < JJ; ++jj) o[jj] = acc[jj][et][r];
     }
 }
 
-// dW_router[i] = sum over chunks in order of part[chunk][i]; four elements per thread.
+// dW_router[o] = sum over chunks of part[chunk][o], in a fixed order: thread (g, o) of a workgroup sums
+// the chunks g, g + 16, g + 32, ... in turn, then the 16 partial sums of an output are added in g order.
+constexpr int RED_G = 16;  // chunk lanes per output
 __global__ __launch_bounds__(256) void route_dw_reduce_kernel(int n4, int nchunks, const float4* __restrict__ part,
                                                               float4* __restrict__ out) {
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += gridDim.x * blockDim.x) {
-    float4 s = part[i];
-    for (int c = 1; c < nchunks; ++c) {
-      const float4 v = part[(size_t)c * n4 + i];
+  __shared__ float4 red[RED_G][256 / RED_G];
+  const int g = threadIdx.x / (256 / RED_G), ol = threadIdx.x % (256 / RED_G);
+  const int o = blockIdx.x * (256 / RED_G) + ol;
+  float4 s = float4{0.f, 0.f, 0.f, 0.f};
+  if (o < n4)
+    for (int c = g; c < nchunks; c += RED_G) {
+      const float4 v = part[(size_t)c * n4 + o];
       s.x += v.x;
       s.y += v.y;
       s.z += v.z;
       s.w += v.w;
     }
-    out[i] = s;
+  red[g][ol] = s;
+  __syncthreads();
+  if (g == 0 && o < n4) {
+    float4 t = red[0][ol];
+    for (int h = 1; h < RED_G; ++h) {
+      const float4 v = red[h][ol];
+      t.x += v.x;
+      t.y += v.y;
+      t.z += v.z;
+      t.w += v.w;
+    }
+    out[o] = t;
   }
 }
 
+static int dw_net(int E) { return E <= 16 ? 1 : E <= 32 ? 2 : E <= 64 ? 4 : E <= 128 ? 8 : 16; }
+
 // Token chunks of the weight-gradient contraction: enough workgroups to fill the chip, chunk sizes a
-// multiple of 32 tokens.
+// multiple of 32 tokens. A workgroup covers 4 wavefronts x 16 x JJ columns.
 static void route_bwd_chunks(const moe_desc& d, int* nch, int* tpc) {
-  const int ncol = d.d_model / 64;
-  const int maxch = (d.T + 63) / 64;
-  int want = (2048 + ncol - 1) / ncol;
+  const int wg_cols = 64 * dw_cols_per_lane(dw_net(d.n_experts));
+  const int ncol = (d.d_model + wg_cols - 1) / wg_cols;
+  const int maxch = (d.T + 31) / 32;
+  int want = (1024 + ncol - 1) / ncol;
   int n = want < maxch ? want : maxch;
   if (n < 1) n = 1;
   int per = (d.T + n - 1) / n;
@@ -339,10 +379,11 @@ static hipError_t route_bwd_t(const moe_desc& d, const void* x, const float* log
   float* part = (float*)ws;
   {
     KernelTimer kt("route_dw_partial", s);
-    dim3 grid(d.d_model / 64, nch);
+    const int wg_cols = 64 * dw_cols_per_lane(dw_net(E));
+    dim3 grid((d.d_model + wg_cols - 1) / wg_cols, nch);
 #define RB_LAUNCH(NET)                                                                                           \
-  hipLaunchKernelGGL((route_dw_partial_kernel<T, NET>), grid, dim3(256), 0, s, d.T, d.d_model, E, tpc,           \
-                     (const T*)x, dl, part)
+  hipLaunchKernelGGL((route_dw_partial_kernel<T, NET, dw_cols_per_lane(NET)>), grid, dim3(256), 0, s, d.T,     \
+                     d.d_model, E, tpc, (const T*)x, dl, part)
     if (E <= 16) RB_LAUNCH(1);
     else if (E <= 32) RB_LAUNCH(2);
     else if (E <= 64) RB_LAUNCH(4);
@@ -353,8 +394,7 @@ static hipError_t route_bwd_t(const moe_desc& d, const void* x, const float* log
   {
     KernelTimer kt("route_dw_reduce", s);
     const int n4 = E * d.d_model / 4;
-    int blocks = (n4 + 255) / 256;
-    if (blocks > 2048) blocks = 2048;
+    const int blocks = (n4 + 256 / RED_G - 1) / (256 / RED_G);
     hipLaunchKernelGGL(route_dw_reduce_kernel, dim3(blocks), dim3(256), 0, s, n4, nch, (const float4*)part,
                        (float4*)dwr);
   }

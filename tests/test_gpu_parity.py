@@ -34,6 +34,9 @@ def small_cases():
     C["k1"] = (LayerConfig("k1", T=256, d=128, f=128, E=4, k=1, seed=16), None)
     C["k_equals_E"] = (LayerConfig("kE", T=256, d=128, f=128, E=4, k=4, seed=17), None)
     C["T1"] = (LayerConfig("t1", T=1, d=128, f=128, E=8, k=2, n_shared=1, seed=18), None)
+    # many experts (router tiles of 8 and 16 expert blocks), k at its maximum, d not a multiple of 512
+    C["E200_k8_d384"] = (LayerConfig("e200", T=512, d=384, f=256, E=200, k=8, seed=23), None)
+    C["E128_f32"] = (LayerConfig("e128", T=256, d=256, f=128, E=128, k=2, dtype="f32", seed=24), None)
 
     def forced_empty(inp):
         inp.logit_bias[0, 3] = -1e4
