@@ -12,128 +12,182 @@ typedef double doublex4 __attribute__((ext_vector_type(4)));
 
 constexpr int RT_TOK = 16;  // tokens per workgroup (one MFMA row block)
 
-// Scores of 16 tokens against all E experts on v_mfma_f64_16x16x4f64. The 4 wavefronts split d into
-// quarters; their fp64 partial sums are added in a fixed order, the bias is added in fp64 and the
+// Scores of 16 tokens against all E experts on v_mfma_f64_16x16x4f64. The W wavefronts split d into
+// W equal ranges; their fp64 partial sums are added in a fixed order, the bias is added in fp64 and the
 // result is rounded once to fp32. Each lane feeds one 16-byte chunk of its token row and of its
 // expert row (8 bf16 / 4 fp32 consecutive k) into 8 / 4 MFMAs: MFMA s takes element s of every
 // lane, so lane group q contributes k = 4*EPC*c + EPC*q + s (the same mapping on both operands).
-// NET = 16-expert tiles per wavefront (E <= 16 * NET).
-template <typename T, int NET>
-__global__ __launch_bounds__(256) void route_fwd_kernel(const T* __restrict__ x, const T* __restrict__ wr,
+// NET = 16-expert tiles per wavefront (E <= 16 * NET). Each wavefront then selects for 16 / W tokens.
+template <typename T, int NET, int W>
+__global__ __launch_bounds__(64 * W) void route_fwd_kernel(const T* __restrict__ x, const T* __restrict__ wr,
                                                         const float* __restrict__ bias, int bias_div, int Tn,
                                                         int d, int E, int k, int renorm,
                                                         float* __restrict__ logits, int32_t* __restrict__ idx,
                                                         float* __restrict__ gw) {
   constexpr int EP = EPC<T>::value;   // elements per 16-byte chunk
   constexpr int EW = 16 * NET + 1;    // padded expert stride of the partial-sum table
-  extern __shared__ double part[];    // [4 waves][16 tokens][EW]
+  extern __shared__ double part[];    // [W waves][16 tokens][EW]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i = lane & 15, q = lane >> 4;
   const int t0 = blockIdx.x * RT_TOK;
   const int t = t0 + i;
-  const int kq = d / 4;
+  const int kq = d / W;
   const int kb = wave * kq;
-  doublex4 acc[NET];
+  // CH independent accumulator chains per expert tile (column steps alternate between them), added in
+  // chain order at the end: back-to-back MFMAs on one accumulator wait for each other.
+  constexpr int CH = NET <= 4 ? 2 : 1;
+  doublex4 acc[CH][NET];
 #pragma unroll
-  for (int et = 0; et < NET; ++et) acc[et] = doublex4{0.0, 0.0, 0.0, 0.0};
+  for (int ch = 0; ch < CH; ++ch)
+#pragma unroll
+    for (int et = 0; et < NET; ++et) acc[ch][et] = doublex4{0.0, 0.0, 0.0, 0.0};
   const T* xrow = x + (size_t)(t < Tn ? t : 0) * d;
-  for (int c = kb; c < kb + kq; c += 4 * EP) {
-    float xf[EP];
-    if (t < Tn) chunk_to_f<T>(ld_chunk(xrow + c + EP * q), xf);
-    else {
-#pragma unroll
-      for (int s = 0; s < EP; ++s) xf[s] = 0.f;
-    }
+  // Column steps of 4 chunks; the loads of the next two steps are in flight while one step computes.
+  const int nstep = kq / (4 * EP);
+  auto load = [&](int st, Chunk& xc, Chunk (&wc)[NET]) {
+    const int c = kb + st * 4 * EP + EP * q;
+    xc = t < Tn ? ld_chunk(xrow + c) : zero_chunk();
 #pragma unroll
     for (int et = 0; et < NET; ++et) {
       const int e = 16 * et + i;
-      float wf[EP];
-      if (e < E) chunk_to_f<T>(ld_chunk(wr + (size_t)e * d + c + EP * q), wf);
-      else {
+      wc[et] = e < E ? ld_chunk(wr + (size_t)e * d + c) : zero_chunk();
+    }
+  };
+  auto compute = [&](const Chunk& xc, const Chunk (&wc)[NET]) {
+    float xf[EP];
+    chunk_to_f<T>(xc, xf);
 #pragma unroll
-        for (int s = 0; s < EP; ++s) wf[s] = 0.f;
-      }
+    for (int et = 0; et < NET; ++et) {
+      float wf[EP];
+      chunk_to_f<T>(wc[et], wf);
 #pragma unroll
       for (int s = 0; s < EP; ++s)
-        acc[et] = __builtin_amdgcn_mfma_f64_16x16x4f64((double)xf[s], (double)wf[s], acc[et], 0, 0, 0);
+        acc[s % CH][et] =
+            __builtin_amdgcn_mfma_f64_16x16x4f64((double)xf[s], (double)wf[s], acc[s % CH][et], 0, 0, 0);
+    }
+  };
+  Chunk xa, xb, wa[NET], wb[NET];
+  if (nstep > 0) load(0, xa, wa);
+  if (nstep > 1) load(1, xb, wb);
+  for (int st = 0; st < nstep; st += 2) {
+    compute(xa, wa);
+    if (st + 2 < nstep) load(st + 2, xa, wa);
+    if (st + 1 < nstep) {
+      compute(xb, wb);
+      if (st + 3 < nstep) load(st + 3, xb, wb);
     }
   }
   // f64 16x16x4 output: register r of lane group q holds D[token 4r + q][expert 16 et + i]
 #pragma unroll
   for (int et = 0; et < NET; ++et)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) part[(wave * 16 + 4 * r + q) * EW + 16 * et + i] = acc[et][r];
+    for (int r = 0; r < 4; ++r) {
+      double a = acc[0][et][r];
+#pragma unroll
+      for (int ch = 1; ch < CH; ++ch) a += acc[ch][et][r];
+      part[(wave * 16 + 4 * r + q) * EW + 16 * et + i] = a;
+    }
   __syncthreads();
 
-  // four tokens per wavefront: fixed-order sum of the quarters, bias, one rounding, then top-k
-  for (int rr = 0; rr < 4; ++rr) {
-    const int row = wave * 4 + rr;
+  // TW tokens per wavefront: fixed-order sum of the W partials, bias, one rounding, then top-k. The
+  // tokens of a wavefront go through the cross-lane argmax rounds together, so their shuffle latencies
+  // overlap.
+  constexpr int TW = RT_TOK / W;  // tokens per wavefront
+  float v[TW][4];
+  bool taken[TW][4];
+#pragma unroll
+  for (int rr = 0; rr < TW; ++rr) {
+    const int row = wave * TW + rr;
     const int tt = t0 + row;
-    if (tt >= Tn) break;
-    float v[4];
-    bool taken[4];
 #pragma unroll
     for (int qq = 0; qq < 4; ++qq) {
       const int e = lane + 64 * qq;
-      v[qq] = -INFINITY;
-      taken[qq] = true;
-      if (e < E) {
-        double sum = part[(0 * 16 + row) * EW + e];
-        sum += part[(1 * 16 + row) * EW + e];
-        sum += part[(2 * 16 + row) * EW + e];
-        sum += part[(3 * 16 + row) * EW + e];
+      v[rr][qq] = -INFINITY;
+      taken[rr][qq] = true;
+      if (tt < Tn && e < E) {
+        double sum = part[row * EW + e];
+#pragma unroll
+        for (int w = 1; w < W; ++w) sum += part[(w * 16 + row) * EW + e];
         if (bias) sum += (double)bias[(size_t)(tt / bias_div) * E + e];
         const float L = (float)sum;
         logits[(size_t)tt * E + e] = L;
-        v[qq] = L;
-        taken[qq] = false;
+        v[rr][qq] = L;
+        taken[rr][qq] = false;
       }
     }
-    float myv = -INFINITY;
-    int myi = 0;
-    for (int j = 0; j < k; ++j) {
-      float bv = -INFINITY;
-      int bi = 0x7fffffff;
+  }
+  float myv[TW], bv[TW];
+  int myi[TW], bi[TW];
+#pragma unroll
+  for (int rr = 0; rr < TW; ++rr) {
+    myv[rr] = -INFINITY;
+    myi[rr] = 0;
+  }
+  for (int j = 0; j < k; ++j) {
+#pragma unroll
+    for (int rr = 0; rr < TW; ++rr) {
+      bv[rr] = -INFINITY;
+      bi[rr] = 0x7fffffff;
 #pragma unroll
       for (int qq = 0; qq < 4; ++qq) {
         const int e = lane + 64 * qq;
-        if (!taken[qq] && (v[qq] > bv || (v[qq] == bv && e < bi))) {
-          bv = v[qq];
-          bi = e;
+        if (!taken[rr][qq] && (v[rr][qq] > bv[rr] || (v[rr][qq] == bv[rr] && e < bi[rr]))) {
+          bv[rr] = v[rr][qq];
+          bi[rr] = e;
         }
+      }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      float ov[TW];
+      int oi[TW];
+#pragma unroll
+      for (int rr = 0; rr < TW; ++rr) {
+        ov[rr] = __shfl_xor(bv[rr], off, 64);
+        oi[rr] = __shfl_xor(bi[rr], off, 64);
       }
 #pragma unroll
-      for (int off = 32; off > 0; off >>= 1) {
-        const float ov = __shfl_xor(bv, off, 64);
-        const int oi = __shfl_xor(bi, off, 64);
-        if (ov > bv || (ov == bv && oi < bi)) {
-          bv = ov;
-          bi = oi;
+      for (int rr = 0; rr < TW; ++rr)
+        if (ov[rr] > bv[rr] || (ov[rr] == bv[rr] && oi[rr] < bi[rr])) {
+          bv[rr] = ov[rr];
+          bi[rr] = oi[rr];
         }
-      }
+    }
+#pragma unroll
+    for (int rr = 0; rr < TW; ++rr) {
 #pragma unroll
       for (int qq = 0; qq < 4; ++qq)
-        if (lane + 64 * qq == bi) taken[qq] = true;
+        if (lane + 64 * qq == bi[rr]) taken[rr][qq] = true;
       if (lane == j) {
-        myv = bv;
-        myi = bi;
+        myv[rr] = bv[rr];
+        myi[rr] = bi[rr];
       }
     }
-    const float m = __shfl(myv, 0, 64);  // the largest score of the token
-    const float ex = (lane < k) ? expf(myv - m) : 0.f;
-    float Z;
+  }
+  float ex[TW], zp[TW];
+#pragma unroll
+  for (int rr = 0; rr < TW; ++rr) {
+    const float m = __shfl(myv[rr], 0, 64);  // the largest score of the token
+    ex[rr] = (lane < k) ? expf(myv[rr] - m) : 0.f;
     if (renorm) {
-      Z = wave_sum(ex);
+      zp[rr] = ex[rr];
     } else {
-      float pz = 0.f;
+      zp[rr] = 0.f;
 #pragma unroll
       for (int qq = 0; qq < 4; ++qq)
-        if (lane + 64 * qq < E) pz += expf(v[qq] - m);
-      Z = wave_sum(pz);
+        if (lane + 64 * qq < E) zp[rr] += expf(v[rr][qq] - m);
     }
-    if (lane < k) {
-      idx[(size_t)tt * k + lane] = myi;
-      gw[(size_t)tt * k + lane] = ex / Z;
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1)
+#pragma unroll
+    for (int rr = 0; rr < TW; ++rr) zp[rr] += __shfl_xor(zp[rr], off, 64);
+#pragma unroll
+  for (int rr = 0; rr < TW; ++rr) {
+    const int tt = t0 + wave * TW + rr;
+    if (tt < Tn && lane < k) {
+      idx[(size_t)tt * k + lane] = myi[rr];
+      gw[(size_t)tt * k + lane] = ex[rr] / zp[rr];
     }
   }
 }
@@ -145,23 +199,42 @@ static hipError_t route_fwd_t(const moe_desc& d, const void* x, const void* wr, 
   dim3 grid((d.T + RT_TOK - 1) / RT_TOK);
   const int div = d.T / (bg > 0 ? bg : 1);
   KernelTimer kt("route_fwd", s);
-#define RT_LAUNCH(NET)                                                                                          \
+  // Wavefronts per workgroup: as many as split d into whole column steps (4 chunks) and keep the
+  // partial-sum table within 64 KB (all 4 beyond that: d is a multiple of 128).
+  constexpr int STEP = 4 * EPC<T>::value;
+  auto waves_for = [&](int net) {
+    for (int wv = 16; wv > 4; wv >>= 1)
+      if (d.d_model % (wv * STEP) == 0 && (size_t)wv * 16 * (16 * net + 1) * sizeof(double) <= 65536) return wv;
+    return 4;
+  };
+#define RT_LAUNCH_W(NET, W)                                                                                     \
   do {                                                                                                          \
-    const size_t lds = (size_t)4 * 16 * (16 * NET + 1) * sizeof(double);                                       \
+    const size_t lds = (size_t)W * 16 * (16 * NET + 1) * sizeof(double);                                       \
     if (lds > 65536) {                                                                                          \
-      hipError_t e_ = hipFuncSetAttribute((const void*)route_fwd_kernel<T, NET>,                                 \
+      hipError_t e_ = hipFuncSetAttribute((const void*)route_fwd_kernel<T, NET, W>,                              \
                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);                \
       if (e_ != hipSuccess) return e_;                                                                          \
     }                                                                                                           \
-    hipLaunchKernelGGL((route_fwd_kernel<T, NET>), grid, dim3(256), lds, s, (const T*)x, (const T*)wr, bias,     \
-                       div, d.T, d.d_model, E, d.top_k, d.renormalize, logits, idx, w);                         \
+    hipLaunchKernelGGL((route_fwd_kernel<T, NET, W>), grid, dim3(64 * W), lds, s, (const T*)x, (const T*)wr,     \
+                       bias, div, d.T, d.d_model, E, d.top_k, d.renormalize, logits, idx, w);                   \
   } while (0)
-  if (E <= 16) RT_LAUNCH(1);
-  else if (E <= 32) RT_LAUNCH(2);
-  else if (E <= 64) RT_LAUNCH(4);
-  else if (E <= 128) RT_LAUNCH(8);
-  else RT_LAUNCH(16);
-#undef RT_LAUNCH
+  // (the table limit leaves 16 wavefronts to NET = 1 and 8 to NET <= 2)
+  if (E <= 16) {
+    const int wv = waves_for(1);
+    if (wv == 16) RT_LAUNCH_W(1, 16);
+    else if (wv == 8) RT_LAUNCH_W(1, 8);
+    else RT_LAUNCH_W(1, 4);
+  } else if (E <= 32) {
+    if (waves_for(2) == 8) RT_LAUNCH_W(2, 8);
+    else RT_LAUNCH_W(2, 4);
+  } else if (E <= 64) {
+    RT_LAUNCH_W(4, 4);
+  } else if (E <= 128) {
+    RT_LAUNCH_W(8, 4);
+  } else {
+    RT_LAUNCH_W(16, 4);
+  }
+#undef RT_LAUNCH_W
   return hipGetLastError();
 }
 

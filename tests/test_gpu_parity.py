@@ -37,6 +37,7 @@ def small_cases():
     # many experts (router tiles of 8 and 16 expert blocks), k at its maximum, d not a multiple of 512
     C["E200_k8_d384"] = (LayerConfig("e200", T=512, d=384, f=256, E=200, k=8, seed=23), None)
     C["E128_f32"] = (LayerConfig("e128", T=256, d=256, f=128, E=128, k=2, dtype="f32", seed=24), None)
+    C["E24_k3"] = (LayerConfig("e24", T=300, d=512, f=256, E=24, k=3, n_shared=1, seed=25), None)
 
     def forced_empty(inp):
         inp.logit_bias[0, 3] = -1e4
