@@ -55,7 +55,7 @@ typedef enum { MOE_F32 = 0, MOE_BF16 = 1 } moe_dtype;
 
 /* Shape of one layer call. */
 typedef struct {
-  int32_t T;            /* tokens in the batch */
+  int32_t T;            /* tokens in the batch, >= 1 (an empty batch is MOE_ERR_INVALID_ARGUMENT) */
   int32_t d_model;      /* hidden size d */
   int32_t d_ff;         /* expert inner size f */
   int32_t n_experts;    /* E: global routed experts = router width (every party owns the whole
@@ -188,6 +188,39 @@ moe_status moe_route_bwd(const moe_desc* desc, const void* x, const float* logit
  */
 moe_status moe_permute_bwd(const moe_desc* desc, const void* dx_perm, const int32_t* slot_to_row,
                            const float* dlogits, const void* w_router, void* dx, hipStream_t stream);
+
+/* Optimiser of the expert update. */
+typedef enum { MOE_OPT_SGD = 0, MOE_OPT_ADAMW = 1 } moe_opt_kind;
+typedef struct {
+  int32_t kind;          /* moe_opt_kind */
+  float lr;              /* learning rate, > 0 */
+  float beta1, beta2;    /* AdamW moment decays, each in [0, 1) */
+  float eps;             /* AdamW denominator term, > 0 */
+  float weight_decay;    /* decoupled decay factor, >= 0 (the parameter shrinks by lr * weight_decay) */
+  int32_t step;          /* AdamW step number t >= 1 (bias corrections 1 - beta^t) */
+} moe_opt;
+
+/*
+ * "Update parameters of E_j" (Alg. 6, the host-side step after BackwardExpert) for every hosted
+ * routed expert and every shared expert, elementwise in fp32:
+ *   SGD:    p <- p - lr * (g + weight_decay * p)
+ *   AdamW:  p <- p * (1 - lr * weight_decay);  m <- beta1 m + (1 - beta1) g;  v <- beta2 v + (1 - beta2) g^2;
+ *           p <- p - lr * (m / (1 - beta1^t)) / (sqrt(v / (1 - beta2^t)) + eps)
+ * The paper leaves the optimiser open; AdamW with decoupled weight decay (Loshchilov & Hutter, ICLR 2019)
+ * and plain SGD are the two offered.
+ *   w_gate, w_up, w_down      the expert weights (layouts of moe_expert_ffn_fwd), dtype, updated in place
+ *   dw_gate, dw_up, dw_down   their gradients (from moe_expert_ffn_bwd), dtype
+ *   master  NULL or fp32 [P]: the master copy of the parameters. When given, the update starts from it,
+ *           it receives the new values and the dtype weights receive their rounding (round to nearest
+ *           even); when NULL the update starts from the dtype weights themselves.
+ *   m, v    fp32 [P] AdamW moments, updated in place (ignored, may be NULL, for SGD)
+ * P = (local_count + n_shared) * 3 * d_ff * d_model; the fp32 arrays hold w_gate, then w_up, then w_down,
+ * each in its own layout. Only the descriptor's expert counts, d_model, d_ff and dtype are used. Errors as
+ * above, and MOE_ERR_INVALID_ARGUMENT for an optimiser setting outside the ranges stated in moe_opt.
+ */
+moe_status moe_expert_update(const moe_desc* desc, const moe_opt* opt, void* w_gate, void* w_up, void* w_down,
+                             const void* dw_gate, const void* dw_up, const void* dw_down, float* master, float* m,
+                             float* v, hipStream_t stream);
 
 /* Per-kernel timing with HIP events recorded around every kernel launch on its own stream
  * (measurement aid; off by default). enable=1 clears the totals and starts recording. */
