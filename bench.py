@@ -112,6 +112,36 @@ def cpu_baseline(cfg, inp, min_seconds=10.0, max_seconds=30.0):
                       f"{total:.1f} s in total", "tokens_per_s": round(cfg.T / dt, 2), "seconds_per_pass": round(dt, 3)}
 
 
+def measure_expert_update(P, layer, w, steps):
+    """The expert update (AdamW with an fp32 master copy) over the hosted experts, timed on its own
+    after the layer steps: HBM bytes per launch = parameters x (weight 2+2, gradient 2, master 4+4,
+    moments 8+8) for bf16 weights."""
+    import torch
+    layer.init_update_state(w, master=True)
+    opt = P.make_opt(kind="adamw", lr=1e-4, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1)
+    for _ in range(2):
+        layer.update(w, opt)
+    torch.cuda.synchronize()
+    P.moe_kernel_timing_select("expert_update")
+    P.moe_kernel_timing(True)
+    n = max(steps // 2, 3)
+    for _ in range(n):
+        layer.update(w, opt)
+    torch.cuda.synchronize()
+    cnt, ms = P.moe_kernel_timing_report()["expert_update"]
+    P.moe_kernel_timing(False)
+    P.moe_kernel_timing_select(None)
+    params = layer.opt_m.numel()
+    es = w.w_gate.element_size()
+    per_param = 3 * es + 8 + 16           # weight read+write, gradient read; master and moments read+write
+    avg_s = ms / cnt / 1e3
+    gbs = params * per_param / avg_s / 1e9
+    return {"kernel": "expert_update", "optimizer": "adamw, fp32 master", "parameters": params,
+            "bytes_per_launch": params * per_param, "avg_launch_us": round(avg_s * 1e6, 2),
+            "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": round(gbs / HBM_PEAK_GBS, 4)}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -217,6 +247,7 @@ def main():
         "kernels_warmup": {k: {"avg_us": round(v["avg_us"], 2), "per_step": v["launches_per_step"]}
                            for k, v in kernels.items()},
     }
+    out["expert_update"] = measure_expert_update(P, layer, w, args.steps)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, inp)
     print(json.dumps(out), flush=True)

@@ -215,8 +215,10 @@ typedef struct {
  *           even); when NULL the update starts from the dtype weights themselves.
  *   m, v    fp32 [P] AdamW moments, updated in place (ignored, may be NULL, for SGD)
  * P = (local_count + n_shared) * 3 * d_ff * d_model; the fp32 arrays hold w_gate, then w_up, then w_down,
- * each in its own layout. Only the descriptor's expert counts, d_model, d_ff and dtype are used. Errors as
- * above, and MOE_ERR_INVALID_ARGUMENT for an optimiser setting outside the ranges stated in moe_opt.
+ * each in its own layout. The descriptor is checked as for the other calls; the update uses its expert
+ * counts, d_model, d_ff and dtype. All pointers 16-byte aligned. Errors as above, and
+ * MOE_ERR_INVALID_ARGUMENT for an optimiser setting outside the ranges stated in moe_opt or a NULL m / v
+ * under AdamW. Calls that overlap on the same parameters race.
  */
 moe_status moe_expert_update(const moe_desc* desc, const moe_opt* opt, void* w_gate, void* w_up, void* w_down,
                              const void* dw_gate, const void* dw_up, const void* dw_down, float* master, float* m,

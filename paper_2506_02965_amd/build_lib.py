@@ -16,7 +16,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libpcmoe.so")
-SOURCES = ["api.hip", "router.hip", "permute.hip", "combine.hip", "grouped_gemm_f32.hip", "grouped_gemm_bf16.hip"]
+SOURCES = ["api.hip", "router.hip", "permute.hip", "combine.hip", "grouped_gemm_f32.hip", "grouped_gemm_bf16.hip",
+           "update.hip"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # packed fp32 instructions are disabled for every device code object of this library

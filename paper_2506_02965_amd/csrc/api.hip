@@ -9,6 +9,7 @@
 #include <cstdio>
 #include <cstring>
 #include <cstdarg>
+#include <cmath>
 
 using namespace pcmoe;
 
@@ -243,6 +244,31 @@ moe_status moe_permute_bwd(const moe_desc* d, const void* dx_perm, const int32_t
   NEED(dx_perm); NEED(slot_to_row); NEED(dx);
   if (dlogits) NEED(w_router);
   return hip_status(launch_permute_bwd(*d, dx_perm, slot_to_row, dlogits, w_router, dx, stream), "moe_permute_bwd");
+}
+
+moe_status moe_expert_update(const moe_desc* d, const moe_opt* opt, void* w_gate, void* w_up, void* w_down,
+                             const void* dw_gate, const void* dw_up, const void* dw_down, float* master, float* m,
+                             float* v, hipStream_t stream) {
+  moe_status st = check_desc(d);
+  if (st) return st;
+  if (!opt) return fail(MOE_ERR_INVALID_ARGUMENT, "opt is NULL");
+  if (opt->kind != MOE_OPT_SGD && opt->kind != MOE_OPT_ADAMW)
+    return fail(MOE_ERR_INVALID_ARGUMENT, "optimiser kind %d", opt->kind);
+  if (!(opt->lr > 0.f) || !std::isfinite(opt->lr)) return fail(MOE_ERR_INVALID_ARGUMENT, "lr must be > 0");
+  if (!(opt->weight_decay >= 0.f) || !std::isfinite(opt->weight_decay))
+    return fail(MOE_ERR_INVALID_ARGUMENT, "weight_decay must be >= 0");
+  NEED(w_gate); NEED(w_up); NEED(w_down); NEED(dw_gate); NEED(dw_up); NEED(dw_down);
+  if (master) NEED(master);
+  if (opt->kind == MOE_OPT_ADAMW) {
+    if (!(opt->beta1 >= 0.f && opt->beta1 < 1.f) || !(opt->beta2 >= 0.f && opt->beta2 < 1.f))
+      return fail(MOE_ERR_INVALID_ARGUMENT, "beta1, beta2 must lie in [0, 1)");
+    if (!(opt->eps > 0.f) || !std::isfinite(opt->eps)) return fail(MOE_ERR_INVALID_ARGUMENT, "eps must be > 0");
+    if (opt->step < 1) return fail(MOE_ERR_INVALID_ARGUMENT, "step must be >= 1");
+    NEED(m); NEED(v);
+  }
+  return hip_status(launch_expert_update(*d, *opt, w_gate, w_up, w_down, dw_gate, dw_up, dw_down, master, m, v,
+                                         stream),
+                    "moe_expert_update");
 }
 
 moe_status moe_kernel_timing(int enable) {

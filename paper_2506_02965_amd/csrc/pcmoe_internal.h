@@ -115,6 +115,9 @@ hipError_t launch_combine(const moe_desc& d, const void* yp, const int32_t* s2r,
 hipError_t launch_combine_bwd(const moe_desc& d, const void* dy, const void* yp, const int32_t* s2r,
                               const float* w, void* dyp, float* dgate, hipStream_t s);
 
+hipError_t launch_expert_update(const moe_desc& d, const moe_opt& o, void* wg, void* wu, void* wd, const void* gg,
+                                const void* gu, const void* gd, float* master, float* m, float* v, hipStream_t s);
+
 size_t ffn_saved_bytes(const moe_desc& d);
 size_t ffn_fwd_ws_bytes(const moe_desc& d);
 size_t ffn_bwd_ws_bytes(const moe_desc& d);

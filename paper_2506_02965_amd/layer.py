@@ -4,6 +4,7 @@ Forward (Alg. 3 with the gating of Alg. 7 and the experts of Alg. 6):
     moe_route -> moe_permute -> moe_expert_ffn_fwd -> moe_combine
 Backward (Alg. 5 / Alg. 6 and the owner-side router adjoint):
     moe_combine_bwd -> moe_expert_ffn_bwd -> moe_route_bwd (full layer only) -> moe_permute_bwd
+Expert update (the last step of Alg. 6): moe_expert_update over the hosted experts' weights.
 All calls are enqueued on one stream; no per-expert count ever returns to the host.
 """
 from __future__ import annotations
@@ -133,6 +134,26 @@ class MoELayer:
             self.route_bwd(w)
         self.permute_bwd(w)
         return self.dx
+
+    # ------------------------------------------------------------- expert update
+    def init_update_state(self, w: LayerWeights, master: bool = True):
+        """fp32 optimiser state over w_gate, w_up, w_down (in that order): zero moments and, if asked,
+        a master copy of the current weights."""
+        n = w.w_gate.numel() + w.w_up.numel() + w.w_down.numel()
+        kw = dict(device=self.device, dtype=torch.float32)
+        self.opt_m = torch.zeros(n, **kw)
+        self.opt_v = torch.zeros(n, **kw)
+        self.opt_master = None
+        if master:
+            self.opt_master = torch.cat([w.w_gate.reshape(-1), w.w_up.reshape(-1), w.w_down.reshape(-1)]).float()
+        self.opt_step = 0
+
+    def update(self, w: LayerWeights, opt: "P.moe_opt"):
+        """One optimiser step of the hosted experts from the gradients of the last backward."""
+        self.opt_step += 1
+        opt.step = self.opt_step
+        P.moe_expert_update(self.desc, opt, w.w_gate, w.w_up, w.w_down, self.dw_gate, self.dw_up, self.dw_down,
+                            self.opt_master, self.opt_m, self.opt_v)
 
     def n_local_rows(self) -> int:
         return int(self.offsets[-1].item())

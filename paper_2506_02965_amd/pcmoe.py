@@ -19,8 +19,9 @@ MOE_WS_PERMUTE, MOE_WS_FFN_SAVED, MOE_WS_FFN_FWD, MOE_WS_FFN_BWD, MOE_WS_ROUTE_B
 
 # every symbol include/pcmoe.h declares
 EXPORTS = ("moe_workspace_size", "moe_route", "moe_permute", "moe_expert_ffn_fwd", "moe_combine", "moe_combine_bwd",
-           "moe_expert_ffn_bwd", "moe_route_bwd", "moe_permute_bwd", "moe_kernel_timing",
+           "moe_expert_ffn_bwd", "moe_route_bwd", "moe_permute_bwd", "moe_expert_update", "moe_kernel_timing",
            "moe_kernel_timing_select", "moe_kernel_timing_report", "moe_status_string", "moe_last_error")
+MOE_OPT_SGD, MOE_OPT_ADAMW = 0, 1
 
 
 class moe_desc(ctypes.Structure):
@@ -28,6 +29,16 @@ class moe_desc(ctypes.Structure):
                 ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32), ("local_begin", ctypes.c_int32),
                 ("local_count", ctypes.c_int32), ("n_shared", ctypes.c_int32), ("renormalize", ctypes.c_int32),
                 ("dtype", ctypes.c_int32)]
+
+
+class moe_opt(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("lr", ctypes.c_float), ("beta1", ctypes.c_float),
+                ("beta2", ctypes.c_float), ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float),
+                ("step", ctypes.c_int32)]
+
+
+def make_opt(kind="adamw", lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, step=1) -> moe_opt:
+    return moe_opt(MOE_OPT_ADAMW if kind == "adamw" else MOE_OPT_SGD, lr, beta1, beta2, eps, weight_decay, step)
 
 
 class MoeError(RuntimeError):
@@ -58,6 +69,7 @@ def lib():
             "moe_expert_ffn_bwd": (_INT, [D] + [_VP] * 14 + [_SZ, _VP]),
             "moe_route_bwd": (_INT, [D, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
             "moe_permute_bwd": (_INT, [D, _VP, _VP, _VP, _VP, _VP, _VP]),
+            "moe_expert_update": (_INT, [D, ctypes.POINTER(moe_opt)] + [_VP] * 9 + [_VP]),
             "moe_kernel_timing": (_INT, [_INT]),
             "moe_kernel_timing_select": (_INT, [ctypes.c_char_p]),
             "moe_kernel_timing_report": (_SZ, [ctypes.c_char_p, _SZ]),
@@ -154,6 +166,13 @@ def moe_route_bwd(desc, x, logits, topk_idx, topk_w, dgate, dlogits, dw_router, 
 def moe_permute_bwd(desc, dx_perm, slot_to_row, dlogits, w_router, dx, stream=None):
     _check("moe_permute_bwd", lib().moe_permute_bwd(ctypes.byref(desc), _ptr(dx_perm), _ptr(slot_to_row),
                                                     _ptr(dlogits), _ptr(w_router), _ptr(dx), _stream(stream)))
+
+
+def moe_expert_update(desc, opt, w_gate, w_up, w_down, dw_gate, dw_up, dw_down, master=None, m=None, v=None,
+                      stream=None):
+    _check("moe_expert_update", lib().moe_expert_update(
+        ctypes.byref(desc), ctypes.byref(opt), _ptr(w_gate), _ptr(w_up), _ptr(w_down), _ptr(dw_gate), _ptr(dw_up),
+        _ptr(dw_down), _ptr(master), _ptr(m), _ptr(v), _stream(stream)))
 
 
 def moe_kernel_timing(enable: bool):

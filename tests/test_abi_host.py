@@ -22,7 +22,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 14, names
+    assert len(names) == 15, names
     assert sorted(P.EXPORTS) == names
     L = P.lib()
     for n in names:
@@ -90,6 +90,34 @@ def test_null_pointers_and_workspace():
     shard = desc(n_experts=8, local_begin=0, local_count=4)
     with pytest.raises(P.MoeError) as ei:
         P.moe_route_bwd(shard, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, stream=0)
+    assert ei.value.status == P.MOE_ERR_INVALID_ARGUMENT
+
+
+@pytest.mark.parametrize("kw,ptrs,status", [
+    (dict(lr=0.0), {}, P.MOE_ERR_INVALID_ARGUMENT),
+    (dict(lr=float("nan")), {}, P.MOE_ERR_INVALID_ARGUMENT),
+    (dict(weight_decay=-1.0), {}, P.MOE_ERR_INVALID_ARGUMENT),
+    (dict(beta1=1.0), {}, P.MOE_ERR_INVALID_ARGUMENT),
+    (dict(beta2=-0.1), {}, P.MOE_ERR_INVALID_ARGUMENT),
+    (dict(eps=0.0), {}, P.MOE_ERR_INVALID_ARGUMENT),
+    (dict(step=0), {}, P.MOE_ERR_INVALID_ARGUMENT),
+    (dict(), dict(m=None), P.MOE_ERR_INVALID_ARGUMENT),            # AdamW needs its moments
+    (dict(), dict(master=FAKE + 8), P.MOE_ERR_INVALID_ARGUMENT),   # misaligned master
+    (dict(kind="sgd", lr=-1.0), dict(m=None, v=None), P.MOE_ERR_INVALID_ARGUMENT),
+])
+def test_update_validation(kw, ptrs, status):
+    args = dict(master=None, m=FAKE, v=FAKE)
+    args.update(ptrs)
+    with pytest.raises(P.MoeError) as ei:
+        P.moe_expert_update(desc(), P.make_opt(**kw), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, stream=0, **args)
+    assert ei.value.status == status
+
+
+def test_update_rejects_bad_kind():
+    o = P.make_opt()
+    o.kind = 7
+    with pytest.raises(P.MoeError) as ei:
+        P.moe_expert_update(desc(), o, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, stream=0)
     assert ei.value.status == P.MOE_ERR_INVALID_ARGUMENT
 
 
