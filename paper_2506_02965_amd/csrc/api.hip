@@ -259,6 +259,9 @@ moe_status moe_expert_update(const moe_desc* d, const moe_opt* opt, void* w_gate
     return fail(MOE_ERR_INVALID_ARGUMENT, "weight_decay must be >= 0");
   NEED(w_gate); NEED(w_up); NEED(w_down); NEED(dw_gate); NEED(dw_up); NEED(dw_down);
   if (master) NEED(master);
+  const int64_t params = (int64_t)(d->local_count + d->n_shared) * d->d_ff * d->d_model;
+  if (params / 8 * 3 / 256 >= ((int64_t)1 << 31) - 1)
+    return fail(MOE_ERR_UNSUPPORTED, "%lld parameters per weight tensor are too many", (long long)params);
   if (opt->kind == MOE_OPT_ADAMW) {
     if (!(opt->beta1 >= 0.f && opt->beta1 < 1.f) || !(opt->beta2 >= 0.f && opt->beta2 < 1.f))
       return fail(MOE_ERR_INVALID_ARGUMENT, "beta1, beta2 must lie in [0, 1)");

@@ -20,12 +20,14 @@ struct UpdateArgs {
   float decay;            // 1 - lr * wd
 };
 
+// One thread per group of 8 consecutive parameters (measured faster than a grid-stride loop over a
+// capped grid).
 template <typename T, bool ADAM, bool MASTER>
 __global__ __launch_bounds__(256) void expert_update_kernel(UpdateArgs a) {
   constexpr int EP = EPC<T>::value;  // elements per 16-byte chunk of the dtype
   const long per = a.n / 8;          // 8-parameter groups per tensor
-  const long total = 3 * per;
-  for (long q = blockIdx.x * (long)blockDim.x + threadIdx.x; q < total; q += (long)gridDim.x * blockDim.x) {
+  const long q = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (q < 3 * per) {
     const int seg = (int)(q / per);
     const long e0 = (q - seg * per) * 8;  // first parameter within the tensor
     const long f0 = seg * a.n + e0;       // and within the fp32 state arrays
@@ -86,8 +88,7 @@ hipError_t launch_expert_update(const moe_desc& d, const moe_opt& o, void* wg, v
   a.inv_sqrt_bc2 = o.kind == MOE_OPT_ADAMW ? (float)(1.0 / sqrt(bc2)) : 0.f;
   a.decay = (float)(1.0 - (double)o.lr * (double)o.weight_decay);
   const long groups = 3 * (a.n / 8);
-  long blocks = (groups + 255) / 256;
-  if (blocks > 4096) blocks = 4096;
+  const long blocks = (groups + 255) / 256;  // < 2^31 (checked by moe_expert_update)
   KernelTimer kt("expert_update", s);
 #define UPD(T, ADAM, MASTER) \
   hipLaunchKernelGGL((expert_update_kernel<T, ADAM, MASTER>), dim3((unsigned)blocks), dim3(256), 0, s, a)
