@@ -142,6 +142,52 @@ def measure_expert_update(P, layer, w, steps):
                          "frac": round(gbs / HBM_PEAK_GBS, 4)}}
 
 
+def memory_amortisation(P, parties=(1, 2, 4, 8)):
+    """The per-party memory claim of Sec. 3 (experts sharded over n parties): one party's peak device memory for
+    the expert layer's training step when it hosts all E experts or E/n of them. The row-space buffers keep their
+    capacity of T*k rows either way, which is what a host receives in expectation from all parties under uniform
+    routing. A shard cannot run the router adjoint (it needs every host's gate gradients), so that one kernel is
+    skipped for n > 1 while its buffers stay allocated. Synthetic inputs; no model or dataset."""
+    import dataclasses
+    import torch
+    from paper_2506_02965_amd.layer import MoELayer, upload, training_footprint
+    from paper_2506_02965_amd.synth import CONFIGS, make_inputs
+    base = dataclasses.replace(CONFIGS[3], bias=None, router_backward=True, local_begin=0)
+    rows = []
+    for n in parties:
+        cfg = dataclasses.replace(base, local_count=base.E // n)
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        start = torch.cuda.memory_allocated()
+        torch.cuda.reset_peak_memory_stats()
+        inp = make_inputs(cfg, with_dy=True)
+        w = upload(inp)
+        del inp
+        layer = MoELayer(cfg, backward=True, router_backward=True)
+        layer.init_update_state(w, master=True)
+        layer.dlogits.zero_()
+        layer.forward(w)
+        layer.combine_bwd(w.dy)
+        layer.ffn_bwd(w, w.dy)
+        if n == 1:
+            layer.route_bwd(w)
+        layer.permute_bwd(w)
+        layer.update(w, P.make_opt(kind="adamw", lr=1e-4, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1))
+        torch.cuda.synchronize()
+        peak = torch.cuda.max_memory_allocated() - start
+        acc = training_footprint(cfg, cfg.n_local)
+        rows.append({"parties": n, "hosted_experts": cfg.n_local, "measured_peak_bytes": int(peak),
+                     "accounted_bytes": acc["total"], "expert_state_bytes": acc["expert_state"],
+                     "activation_bytes": acc["activations"], "owner_bytes": acc["owner"]})
+        del layer, w
+    full = rows[0]["measured_peak_bytes"]
+    for r in rows:
+        r["relative_to_all_experts"] = round(r["measured_peak_bytes"] / full, 4)
+    return {"experiment": "per-party memory of the expert layer's training step, experts sharded over n parties",
+            "workload": "T=8192 d=2048 f=1408 E=64 top-4, bf16, AdamW with fp32 master and moments",
+            "data": "synthetic", "rows": rows}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -149,6 +195,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--memory", action="store_true",
+                    help="instead of the benchmark: peak device memory of one party's expert-layer training step "
+                         "(fwd, bwd, AdamW update) hosting all 64 experts of the T=8192/d=2048/f=1408/E=64/k=4 "
+                         "layer or 1/n of them (n = 2, 4, 8 parties), measured and accounted")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="before the warm-up, copy a 256 MiB device buffer three times (the reference kernel "
                          "that scales the HBM byte counters of a rocprofv3 --pmc run)")
@@ -164,6 +214,9 @@ def main():
     from paper_2506_02965_amd.synth import CONFIGS, make_inputs
 
     P.lib()
+    if args.memory:
+        print(json.dumps(memory_amortisation(P)), flush=True)
+        return
     if args.copy_calibration:
         src = torch.ones(COPY_CAL_BYTES // 4, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)

@@ -144,8 +144,12 @@ class MoELayer:
         self.opt_m = torch.zeros(n, **kw)
         self.opt_v = torch.zeros(n, **kw)
         self.opt_master = None
-        if master:
-            self.opt_master = torch.cat([w.w_gate.reshape(-1), w.w_up.reshape(-1), w.w_down.reshape(-1)]).float()
+        if master:  # filled slice by slice: no transient copy of all parameters
+            self.opt_master = torch.empty(n, **kw)
+            o = 0
+            for t in (w.w_gate, w.w_up, w.w_down):
+                self.opt_master[o:o + t.numel()].copy_(t.reshape(-1))
+                o += t.numel()
         self.opt_step = 0
 
     def update(self, w: LayerWeights, opt: "P.moe_opt"):
@@ -157,3 +161,34 @@ class MoELayer:
 
     def n_local_rows(self) -> int:
         return int(self.offsets[-1].item())
+
+
+def training_footprint(cfg, local_count: int, master: bool = True) -> dict:
+    """Device bytes one party allocates for the expert layer's training step (route, permute, expert FFN forward
+    and backward, combine and its adjoint, router adjoint, expert AdamW update) when it hosts `local_count` of the
+    cfg.E routed experts, by category:
+      expert_state  hosted experts' weights and weight gradients (dtype) plus fp32 moments and master copy;
+      activations   row-space buffers (capacity T*k + S*T rows), saved activations and the FFN workspaces;
+      owner         the owner-side buffers of its own T tokens (input, router, combine, input gradient).
+    The sizes are those MoELayer and init_update_state allocate, with workspace sizes from the library."""
+    T, d, f, E, k, S = cfg.T, cfg.d, cfg.f, cfg.E, cfg.k, cfg.n_shared
+    es = 2 if cfg.dtype == "bf16" else 4
+    desc = P.make_desc(T, d, f, E, k, 0, local_count, S, cfg.renormalize, cfg.dtype)
+    ws = lambda which: max(P.moe_workspace_size(desc, which), 1)
+    G, R = local_count + S, T * k + S * T
+    params = G * 3 * f * d
+    expert_state = params * es * 2 + params * 4 * (3 if master else 2)
+    activations = (T * k * d * es            # x_perm
+                   + R * d * es              # y_perm
+                   + T * k * d * es          # dy_perm
+                   + R * d * es              # dx_perm
+                   + ws(P.MOE_WS_FFN_SAVED) + ws(P.MOE_WS_FFN_FWD) + ws(P.MOE_WS_FFN_BWD) + ws(P.MOE_WS_PERMUTE)
+                   + (local_count + 1) * 4 + max(local_count, 1) * 4 + 2 * T * k * 4)   # offsets, counts, maps
+    owner = (T * d * es * 3                  # x, y, dx
+             + T * d * es                    # dy
+             + E * d * es + E * d * 4        # router weights and their gradient
+             + T * E * 4 * 2                 # logits, dlogits
+             + T * k * (4 + 4 + 4)           # topk_idx, topk_w, dgate
+             + ws(P.MOE_WS_ROUTE_BWD))
+    return {"local_experts": local_count, "expert_state": expert_state, "activations": activations, "owner": owner,
+            "total": expert_state + activations + owner}

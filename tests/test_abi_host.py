@@ -126,3 +126,17 @@ def test_timing_report_empty():
     P.moe_kernel_timing_select("gemm_bwd_dx")
     P.moe_kernel_timing_select(None)
     assert P.moe_kernel_timing_report() == {}
+
+
+def test_training_footprint_scales_expert_state_only():
+    """One party's expert-layer memory: the hosted experts' state scales with the number hosted, the row-space
+    buffers do not (their capacity is T*k rows either way)."""
+    import dataclasses
+    from paper_2506_02965_amd.layer import training_footprint
+    from paper_2506_02965_amd.synth import CONFIGS
+    cfg = dataclasses.replace(CONFIGS[3], bias=None, router_backward=True, local_begin=0)
+    f64, f8 = training_footprint(cfg, 64), training_footprint(cfg, 8)
+    assert f64["expert_state"] == 8 * f8["expert_state"]
+    assert f64["expert_state"] == 64 * 3 * 1408 * 2048 * (2 + 2 + 12)
+    assert abs(f64["activations"] - f8["activations"]) < 1e-3 * f64["activations"]
+    assert f64["owner"] == f8["owner"]
