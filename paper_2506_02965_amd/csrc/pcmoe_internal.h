@@ -20,11 +20,13 @@ struct __align__(16) Chunk {
 __device__ __forceinline__ float bf2f(bf16 v) { return __uint_as_float(((uint32_t)v) << 16); }
 
 // float -> bfloat16, round to nearest, ties to even (finite values).
-__device__ __forceinline__ bf16 f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16)(u >> 16);
+// fp32 -> bf16, round to nearest even: one v_cvt_pk_bf16_f32 per pair of values on gfx950.
+typedef __bf16 bf16x2_hw __attribute__((ext_vector_type(2)));
+typedef float floatx2_hw __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((floatx2_hw){lo, hi}, bf16x2_hw));
 }
+__device__ __forceinline__ bf16 f2bf(float f) { return (bf16)(pack_bf16x2(f, 0.f) & 0xffffu); }
 
 __device__ __forceinline__ float to_f(float v) { return v; }
 __device__ __forceinline__ float to_f(bf16 v) { return bf2f(v); }
@@ -60,7 +62,7 @@ template <> __device__ __forceinline__ Chunk f_to_chunk<float>(const float* in) 
 template <> __device__ __forceinline__ Chunk f_to_chunk<bf16>(const float* in) {
   Chunk c;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) c.w[i] = (uint32_t)f2bf(in[2 * i]) | ((uint32_t)f2bf(in[2 * i + 1]) << 16);
+  for (int i = 0; i < 4; ++i) c.w[i] = pack_bf16x2(in[2 * i], in[2 * i + 1]);
   return c;
 }
 
