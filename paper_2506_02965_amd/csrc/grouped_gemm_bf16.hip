@@ -98,6 +98,10 @@ __device__ __forceinline__ void mfma_bf16(floatx4& acc, const Chunk& a, const Ch
                                                 0, 0);
 }
 
+// Logistic sigmoid for epilogues whose results are rounded to bf16: hardware exp and reciprocal (about
+// 1 ulp of fp32 each) instead of an IEEE division; saturates to 0 and 1 at the tails.
+__device__ __forceinline__ float sigmoid_bf16_out(float x) { return __builtin_amdgcn_rcpf(1.f + __expf(-x)); }
+
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
@@ -351,7 +355,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
         chunk_to_f<bf16>(uch[it], uv);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float sg = 1.f / (1.f + __expf(-gv[e]));
+          const float sg = sigmoid_bf16_out(gv[e]);
           du[e] = v[e] * gv[e] * sg;
           dg[e] = v[e] * uv[e] * sg * (1.f + gv[e] * (1.f - sg));
         }
@@ -374,7 +378,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           u[e] = st[rr * C::PITCH + OUT_W + cc + e];
-          const float sg = 1.f / (1.f + __expf(-v[e]));
+          const float sg = sigmoid_bf16_out(v[e]);
           hv[e] = v[e] * sg * u[e];
         }
         const int col = ti.nt * (BN / 2) + wn * OUT_W + cc;
