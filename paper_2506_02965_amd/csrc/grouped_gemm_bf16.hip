@@ -520,16 +520,18 @@ static long mtile_bound2(const moe_desc& d, int bm) {
   return routed + (long)d.n_shared * ((d.T + bm - 1) / bm);
 }
 
-size_t ffn_saved_bytes(const moe_desc& d) {
+static size_t plan_part(const moe_desc& d) { return align256((size_t)(d.local_count + d.n_shared + 1) * 4); }
+static size_t plan_bytes(const moe_desc& d) { return 3 * plan_part(d); }
+// saved = G|U [R, 2f], H [R, f], then the tile plan of the forward, which the backward reuses
+static size_t saved_plan_offset(const moe_desc& d) {
   const size_t R = (size_t)rows_total(d), es = elem_bytes(d);
   return align256(R * 2 * d.d_ff * es) + align256(R * d.d_ff * es);
 }
-static size_t plan_part(const moe_desc& d) { return align256((size_t)(d.local_count + d.n_shared + 1) * 4); }
-static size_t plan_bytes(const moe_desc& d) { return 3 * plan_part(d); }
-size_t ffn_fwd_ws_bytes(const moe_desc& d) { return plan_bytes(d); }
+size_t ffn_saved_bytes(const moe_desc& d) { return saved_plan_offset(d) + plan_bytes(d); }
+size_t ffn_fwd_ws_bytes(const moe_desc&) { return 0; }
 size_t ffn_bwd_ws_bytes(const moe_desc& d) {
   const size_t R = (size_t)rows_total(d), es = elem_bytes(d);
-  return align256(R * 2 * d.d_ff * es) + plan_bytes(d);
+  return align256(R * 2 * d.d_ff * es);
 }
 
 struct Plan {
@@ -538,12 +540,16 @@ struct Plan {
   int32_t* order;
 };
 
-// m-tile prefixes for 128- and 256-row tiles and the heaviest-first group order
-static Plan plan(const moe_desc& d, const int32_t* offsets, void* where, hipStream_t s) {
+// The plan's arrays at `where`: m-tile prefixes for 128- and 256-row tiles and the heaviest-first group order.
+static Plan plan_at(const moe_desc& d, void* where) {
   Plan pl;
   pl.pre128 = (int32_t*)where;
   pl.pre256 = (int32_t*)((char*)where + plan_part(d));
   pl.order = (int32_t*)((char*)where + 2 * plan_part(d));
+  return pl;
+}
+static Plan plan(const moe_desc& d, const int32_t* offsets, void* where, hipStream_t s) {
+  Plan pl = plan_at(d, where);
   KernelTimer kt("ffn_plan", s);
   hipLaunchKernelGGL(mtile_prefix_kernel, dim3(1), dim3(512), 0, s, offsets, d.local_count, d.n_shared, d.T, 128, 256,
                      pl.pre128, pl.pre256, pl.order);
@@ -630,8 +636,8 @@ static hipError_t run_pair(const Prep& A, const Prep& B, hipStream_t s, const ch
 }
 
 hipError_t launch_ffn_fwd(const moe_desc& d, const void* x, const void* xp, const int32_t* offsets, const void* wg,
-                          const void* wu, const void* wd, void* yp, void* saved, void* ws, hipStream_t s) {
-  Plan pl = plan(d, offsets, ws, s);
+                          const void* wu, const void* wd, void* yp, void* saved, void*, hipStream_t s) {
+  Plan pl = plan(d, offsets, (char*)saved + saved_plan_offset(d), s);
   if (d.dtype != MOE_BF16) return ffn_fwd_f32(d, x, xp, offsets, wg, wu, wd, yp, saved, pl.pre128, s);
   const size_t R = (size_t)rows_total(d);
   GemmArgs a = args_for(d, offsets);
@@ -649,7 +655,8 @@ hipError_t launch_ffn_bwd(const moe_desc& d, const void* x, const void* xp, cons
                           void* dxp, void* dwg, void* dwu, void* dwd, void* ws, hipStream_t s) {
   const size_t R = (size_t)rows_total(d), es = elem_bytes(d);
   void* dgu = ws;
-  Plan pl = plan(d, offsets, (char*)ws + align256(R * 2 * d.d_ff * es), s);
+  (void)es;
+  Plan pl = plan_at(d, (char*)saved + saved_plan_offset(d));  // written by the forward for the same offsets
   if (d.dtype != MOE_BF16)
     return ffn_bwd_f32(d, x, xp, dy, dyp, offsets, wg, wu, wd, saved, dxp, dwg, dwu, dwd, dgu, pl.pre128, s);
   GemmArgs a = args_for(d, offsets);

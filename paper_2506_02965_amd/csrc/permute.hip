@@ -4,10 +4,11 @@
 //
 // Ordering is reproducible bit for bit: rows of one expert are in increasing slot order.
 //   1. histogram: per block of PM_SLOTS slots, per hosted expert counts (LDS atomics; order-free)
-//   2. scan: per expert, exclusive prefix over blocks, then over experts -> offsets
-//   3. scatter: inside a block, each wavefront ranks its 64 slots with ballots (lanes holding
-//      the same expert form a peer mask; rank = popcount of lower peers), waves in order.
-//   4. gather: one wavefront per token reads its row once and writes its k destinations.
+//   2. scatter: each block first derives its own base per expert from the histogram (the exclusive
+//      prefix over experts of the totals, plus the counts of the earlier blocks; block 0 also writes
+//      counts and offsets), then each wavefront ranks its 64 slots with ballots (lanes holding the
+//      same expert form a peer mask; rank = popcount of lower peers), waves in order.
+//   3. gather: one wavefront per token reads its row once and writes its k destinations.
 #include "pcmoe_internal.h"
 
 namespace pcmoe {
@@ -41,52 +42,47 @@ __global__ __launch_bounds__(256) void perm_hist_kernel(const int32_t* __restric
   for (int e = threadIdx.x; e < lc; e += 256) blk_counts[(size_t)blockIdx.x * lc + e] = hist[e];
 }
 
-// One block: per-expert totals, offsets and per-(block, expert) bases.
-__global__ __launch_bounds__(256) void perm_scan_kernel(int nblk, int lc, const int32_t* __restrict__ blk_counts,
-                                                        int32_t* __restrict__ blk_base, int32_t* __restrict__ counts,
-                                                        int32_t* __restrict__ offsets) {
-  __shared__ int tot[256];
-  __shared__ int wsum[4];
-  const int e = threadIdx.x;
-  int run = 0;
-  if (e < lc)
-    for (int b = 0; b < nblk; ++b) run += blk_counts[(size_t)b * lc + e];
-  tot[e] = (e < lc) ? run : 0;
-  __syncthreads();
-  // exclusive scan of tot[0..255] (lc <= 256)
-  const int lane = e & 63, w = e >> 6;
-  int v = tot[e];
-  int incl = v;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    int o = __shfl_up(incl, off, 64);
-    if (lane >= off) incl += o;
-  }
-  if (lane == 63) wsum[w] = incl;
-  __syncthreads();
-  int base = 0;
-  for (int i = 0; i < w; ++i) base += wsum[i];
-  const int excl = base + incl - v;
-  if (e < lc) {
-    counts[e] = v;
-    offsets[e] = excl;
-    int r = excl;
-    for (int b = 0; b < nblk; ++b) {
-      blk_base[(size_t)b * lc + e] = r;
-      r += blk_counts[(size_t)b * lc + e];
-    }
-  }
-  if (e == lc - 1) offsets[lc] = excl + v;
-}
-
 __global__ __launch_bounds__(256) void perm_scatter_kernel(const int32_t* __restrict__ idx, int nslots, int lb,
-                                                           int lc, int nbits,
-                                                           const int32_t* __restrict__ blk_base,
-                                                           const int32_t* __restrict__ offsets,
+                                                           int lc, int nbits, int nblk,
+                                                           const int32_t* __restrict__ blk_counts,
+                                                           int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
                                                            int32_t* __restrict__ r2s, int32_t* __restrict__ s2r) {
   extern __shared__ int wcnt[];  // [4][lc]
+  __shared__ int base[256];      // this block's first row per expert
+  __shared__ int wsum[4];
+  __shared__ int nloc_s;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   for (int i = threadIdx.x; i < 4 * lc; i += 256) wcnt[i] = 0;
+  {
+    // expert e = thread: its total and the rows of the earlier blocks, then the exclusive prefix of the
+    // totals over experts (lc <= 256)
+    const int e = threadIdx.x;
+    int tot = 0, before = 0;
+    if (e < lc)
+      for (int b = 0; b < nblk; ++b) {
+        const int c = blk_counts[(size_t)b * lc + e];
+        if (b < (int)blockIdx.x) before += c;
+        tot += c;
+      }
+    int incl = tot;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int o = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += o;
+    }
+    if (lane == 63) wsum[w] = incl;
+    __syncthreads();
+    int wb = 0;
+    for (int i = 0; i < w; ++i) wb += wsum[i];
+    const int excl = wb + incl - tot;
+    base[e] = excl + before;
+    if (e == 255) nloc_s = wb + incl;  // rows of all hosted experts
+    if (blockIdx.x == 0 && e < lc) {
+      counts[e] = tot;
+      offsets[e] = excl;
+      if (e == lc - 1) offsets[lc] = excl + tot;
+    }
+  }
   __syncthreads();
   const int a_w = blockIdx.x * PM_SLOTS + w * (PM_SLOTS / 4);
   const uint64_t lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
@@ -102,7 +98,7 @@ __global__ __launch_bounds__(256) void perm_scatter_kernel(const int32_t* __rest
   }
   __syncthreads();
   for (int e = threadIdx.x; e < lc; e += 256) {
-    int r = blk_base[(size_t)blockIdx.x * lc + e];
+    int r = base[e];
     for (int ww = 0; ww < 4; ++ww) {
       int c = wcnt[ww * lc + e];
       wcnt[ww * lc + e] = r;
@@ -130,7 +126,7 @@ __global__ __launch_bounds__(256) void perm_scatter_kernel(const int32_t* __rest
     if (loc && (peers & lt) == 0) mine[v] += __popcll(peers);
   }
   // rows beyond N_loc have no slot
-  const int nloc = offsets[lc];
+  const int nloc = nloc_s;
   for (int i = threadIdx.x; i < PM_SLOTS; i += 256) {
     int r = blockIdx.x * PM_SLOTS + i;
     if (r < nslots && r >= nloc) r2s[r] = -1;
@@ -165,7 +161,7 @@ static int nbits_for(int lc) {
 size_t permute_ws_bytes(const moe_desc& d) {
   size_t nslots = (size_t)d.T * d.top_k;
   size_t nblk = (nslots + PM_SLOTS - 1) / PM_SLOTS;
-  return 2 * align256(nblk * d.local_count * sizeof(int32_t));
+  return align256(nblk * d.local_count * sizeof(int32_t));
 }
 
 static int gather_blocks(int Tn) {
@@ -179,20 +175,15 @@ hipError_t launch_permute(const moe_desc& d, const int32_t* idx, const void* x, 
   const int nblk = (nslots + PM_SLOTS - 1) / PM_SLOTS;
   const int lc = d.local_count;
   int32_t* blk_counts = (int32_t*)ws;
-  int32_t* blk_base = (int32_t*)((char*)ws + align256((size_t)nblk * lc * sizeof(int32_t)));
   {
     KernelTimer kt("permute_hist", s);
     hipLaunchKernelGGL(perm_hist_kernel, dim3(nblk), dim3(256), lc * sizeof(int), s, idx, nslots, d.local_begin, lc,
                        blk_counts);
   }
   {
-    KernelTimer kt("permute_scan", s);
-    hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(256), 0, s, nblk, lc, blk_counts, blk_base, counts, offsets);
-  }
-  {
     KernelTimer kt("permute_scatter", s);
     hipLaunchKernelGGL(perm_scatter_kernel, dim3(nblk), dim3(256), 4 * lc * sizeof(int), s, idx, nslots,
-                       d.local_begin, lc, nbits_for(lc), blk_base, offsets, r2s, s2r);
+                       d.local_begin, lc, nbits_for(lc), nblk, blk_counts, counts, offsets, r2s, s2r);
   }
   {
     KernelTimer kt("permute_gather", s);
