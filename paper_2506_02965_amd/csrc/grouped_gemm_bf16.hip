@@ -57,12 +57,17 @@ __device__ __forceinline__ void dma16(int32x4 rsrc, uint32_t m0, int voff) {
 
 // K-contiguous tile rows of BK bf16 (BK = 64: 8 chunks of 16 bytes; BK = 32: 4 chunks): chunk c of row r
 // lives at chunk c ^ kc_swz(r). With the two 8-byte halves read by alternating lane groups, 16 rows of
-// one chunk column then cover every bank once per LDS pass.
+// one chunk column then cover every bank once per LDS pass. The swizzle depends on row bits 0..3 only,
+// and every 16 rows are followed by 16 bytes of padding (kc_row): a fragment 16 rows further is then
+// at the same lane address plus an immediate offset (16 * ROWB + 16) that the compiler cannot fuse
+// with its neighbour's read into one ds_read2 (which would need register moves to split again).
 template <int BK>
 __device__ __forceinline__ int kc_swz(int r) {
-  if (BK == 64) return (r ^ (r >> 3)) & 7;
+  if (BK == 64) return (r & 7) ^ ((r >> 3) & 1);
   return (r >> 2) & 3;
 }
+template <int ROWB>
+__device__ __forceinline__ int kc_row(int r) { return r * ROWB + 16 * (r >> 4); }
 // K-major tile rows (R*2 bytes): 16-byte chunk c of k-row k lives at chunk c ^ mc_swz(k).
 __device__ __forceinline__ int mc_swz(int k) { return ((k & 3) << 1) | (((k >> 3) & 1) << 3); }
 
@@ -118,7 +123,8 @@ struct Cfg2 {
   static constexpr int CR = ROWB / 16;             // 16-byte chunks per K-contiguous row
   static constexpr int RPI = 1024 / ROWB;          // K-contiguous rows per direct-load instruction
   static constexpr int KK = BK / 32;               // MFMA k-steps per K-tile
-  static constexpr int STAGE_BYTES = (BM + BN) * ROWB;
+  static constexpr int A_BYTES = BM * ROWB + BM;  // K-contiguous layouts pad 16 bytes per 16 rows
+  static constexpr int STAGE_BYTES = A_BYTES + BN * ROWB + BN;
   static constexpr int LDS_MAIN = STAGES * STAGE_BYTES;
   static constexpr int PART_ROWS = WTM < 32 ? WTM : 32;
   static constexpr int PITCH = WTN + 4;  // fp32 epilogue staging pitch
@@ -237,18 +243,21 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
   const uint32_t lds0 = lds_addr(smem) + wave * 1024;
   auto issue_one = [&](int kt, int stage, int idx) {
     const uint32_t As = lds0 + stage * C::STAGE_BYTES;
-    const uint32_t Bs = As + BM * C::ROWB;
+    const uint32_t Bs = As + C::A_BYTES;
     const int k0 = kt * BK;
+    // instruction jj = wave + NW * j fills K-contiguous rows RPI * jj .. RPI * jj + RPI - 1
+    const auto pad = [&](int j) { return 16 * ((C::RPI * (wave + C::NW * j)) >> 4); };
     if (idx < C::IA) {
       const int j = idx;
-      dma16(ra, As + C::NW * j * 1024, va[j] + (KT::a_kc ? k0 * ES : k0 * a_ld));
+      dma16(ra, As + C::NW * j * 1024 + (KT::a_kc ? pad(j) : 0), va[j] + (KT::a_kc ? k0 * ES : k0 * a_ld));
     } else {
       const int j = idx - C::IA;
       if (KIND == BWD_DX) {
         const bool up = k0 >= f;
         dma16(up ? rb1 : rb0, Bs + C::NW * j * 1024, vb[j] + (up ? k0 - f : k0) * b_ld);
       } else {
-        dma16(bup[j] ? rb1 : rb0, Bs + C::NW * j * 1024, vb[j] + (KT::b_kc ? k0 * ES : k0 * b_ld));
+        dma16(bup[j] ? rb1 : rb0, Bs + C::NW * j * 1024 + (KT::b_kc ? pad(j) : 0),
+              vb[j] + (KT::b_kc ? k0 * ES : k0 * b_ld));
       }
     }
   };
@@ -278,15 +287,18 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     if (kt + STAGES - 1 < KTN) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
     const char* As = smem + (kt % STAGES) * C::STAGE_BYTES;
-    const char* Bs = As + BM * C::ROWB;
+    const char* Bs = As + C::A_BYTES;
 #pragma unroll
     for (int kk = 0; kk < C::KK; ++kk) {
       Chunk a[C::FM], b[C::FN];
+      // K-contiguous fragments: row 16 * i + li of the wave's rows; the swizzle sees only li, and
+      // fragment i sits FRAG bytes after fragment 0 (an immediate offset of the LDS read)
+      constexpr int FRAG = 16 * C::ROWB + 16;
+      const int lane_kc = li * C::ROWB + (((4 * kk + q) ^ kc_swz<BK>(li)) << 4);
 #pragma unroll
       for (int i = 0; i < C::FM; ++i) {
         if (KT::a_kc) {
-          const int r = wm * C::WTM + 16 * i + li, c = 4 * kk + q;
-          a[i] = lds_kc_pair(As + r * C::ROWB + ((c ^ kc_swz<BK>(r)) << 4), q);
+          a[i] = lds_kc_pair(As + kc_row<C::ROWB>(wm * C::WTM) + lane_kc + i * FRAG, q);
         } else {
           const int k1 = 32 * kk + 8 * q + 4 * (q & 1) + (li >> 2), mn = wm * C::WTM + 16 * i + 4 * (li & 3);
           const int k2 = k1 + 4 - 8 * (q & 1);
@@ -297,8 +309,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
 #pragma unroll
       for (int j = 0; j < C::FN; ++j) {
         if (KT::b_kc) {
-          const int r = wn * C::WTN + 16 * j + li, c = 4 * kk + q;
-          b[j] = lds_kc_pair(Bs + r * C::ROWB + ((c ^ kc_swz<BK>(r)) << 4), q);
+          b[j] = lds_kc_pair(Bs + kc_row<C::ROWB>(wn * C::WTN) + lane_kc + j * FRAG, q);
         } else {
           const int k1 = 32 * kk + 8 * q + 4 * (q & 1) + (li >> 2), mn = wn * C::WTN + 16 * j + 4 * (li & 3);
           const int k2 = k1 + 4 - 8 * (q & 1);
