@@ -70,6 +70,12 @@ template <int ROWB>
 __device__ __forceinline__ int kc_row(int r) { return r * ROWB + 16 * (r >> 4); }
 // K-major tile rows (R*2 bytes): 16-byte chunk c of k-row k lives at chunk c ^ mc_swz(k).
 __device__ __forceinline__ int mc_swz(int k) { return ((k & 3) << 1) | (((k >> 3) & 1) << 3); }
+// K-major tiles 256 wide read by 64-wide wave tiles use a padded layout instead: 512-byte rows two to
+// a 1 KB direct-load block, each block followed by 32 bytes of padding, odd rows rotated by 8 chunks.
+// The 8 rows one ds_read_b64_tr_b16 pass touches then fall on 8 distinct 32-byte bank groups, and a
+// lane's address for fragment i and k-step kk is its fragment-0 address plus 32 i + 16896 kk.
+constexpr int MK_BLOCK = 1056;
+__device__ __forceinline__ int mk_row(int k) { return (k >> 1) * MK_BLOCK + (k & 1) * 512; }
 
 // A K-contiguous operand fragment as two 8-byte reads. Lane groups with odd q read the upper half of
 // their 16-byte chunk first, so that the 32 lanes of one LDS pass cover all banks; the MFMA then sees
@@ -123,8 +129,11 @@ struct Cfg2 {
   static constexpr int CR = ROWB / 16;             // 16-byte chunks per K-contiguous row
   static constexpr int RPI = 1024 / ROWB;          // K-contiguous rows per direct-load instruction
   static constexpr int KK = BK / 32;               // MFMA k-steps per K-tile
-  static constexpr int A_BYTES = BM * ROWB + BM;  // K-contiguous layouts pad 16 bytes per 16 rows
-  static constexpr int STAGE_BYTES = A_BYTES + BN * ROWB + BN;
+  // padding: 16 bytes per 16 K-contiguous rows, or 32 bytes per 1 KB block of a padded K-major tile
+  static constexpr int PAD_A = (BM > 32 * (BM * ROWB / 1024) ? BM : 32 * (BM * ROWB / 1024));
+  static constexpr int PAD_B = (BN > 32 * (BN * ROWB / 1024) ? BN : 32 * (BN * ROWB / 1024));
+  static constexpr int A_BYTES = BM * ROWB + PAD_A;
+  static constexpr int STAGE_BYTES = A_BYTES + BN * ROWB + PAD_B;
   static constexpr int LDS_MAIN = STAGES * STAGE_BYTES;
   static constexpr int PART_ROWS = WTM < 32 ? WTM : 32;
   static constexpr int PITCH = WTN + 4;  // fp32 epilogue staging pitch
@@ -201,6 +210,10 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
     b_ld = d * ES;
   }
 
+  // K-major operands in the padded layout (mk_row)
+  constexpr bool MKP_A = !KT::a_kc && BM == 256 && C::WTM == 64;
+  constexpr bool MKP_B = !KT::b_kc && BN == 256 && C::WTN == 64;
+
   // per-lane byte offsets of each direct-load instruction at K-tile 0
   int va[C::IA], vb[C::IB];
   bool bup[C::IB];  // FWD_GU: instruction reads W_up rows
@@ -210,6 +223,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
     if (KT::a_kc) {
       const int r = C::RPI * jj + lane / C::CR, c = (lane % C::CR) ^ kc_swz<BK>(r);
       va[j] = (m0 + r) * a_ld + 16 * c;
+    } else if (MKP_A) {
+      const int kr = 2 * jj + (lane >> 5), c = ((lane & 31) - 8 * (kr & 1)) & 31;
+      va[j] = kr * a_ld + (m0 + 8 * c) * ES;
     } else {
       constexpr int CPR = BM / 8;
       const int slot = 64 * jj + lane, kr = slot / CPR, c = (slot % CPR) ^ mc_swz(kr);
@@ -232,6 +248,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
         wrow = n0 + r;
       }
       vb[j] = wrow * b_ld + 16 * c;
+    } else if (MKP_B) {
+      const int kr = 2 * jj + (lane >> 5), c = ((lane & 31) - 8 * (kr & 1)) & 31;
+      vb[j] = kr * b_ld + (n0 + 8 * c) * ES;
     } else {
       constexpr int CPR = BN / 8;
       const int slot = 64 * jj + lane, kr = slot / CPR, c = (slot % CPR) ^ mc_swz(kr);
@@ -245,18 +264,22 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
     const uint32_t As = lds0 + stage * C::STAGE_BYTES;
     const uint32_t Bs = As + C::A_BYTES;
     const int k0 = kt * BK;
-    // instruction jj = wave + NW * j fills K-contiguous rows RPI * jj .. RPI * jj + RPI - 1
-    const auto pad = [&](int j) { return 16 * ((C::RPI * (wave + C::NW * j)) >> 4); };
+    // padding before instruction jj = wave + NW * j: K-contiguous rows RPI * jj .. RPI * jj + RPI - 1
+    // follow 16 bytes per earlier 16 rows; a padded K-major block follows 32 bytes per earlier block
+    const auto pad = [&](int j, bool kc, bool mkp) {
+      const int jj = wave + C::NW * j;
+      return kc ? 16 * ((C::RPI * jj) >> 4) : (mkp ? 32 * jj : 0);
+    };
     if (idx < C::IA) {
       const int j = idx;
-      dma16(ra, As + C::NW * j * 1024 + (KT::a_kc ? pad(j) : 0), va[j] + (KT::a_kc ? k0 * ES : k0 * a_ld));
+      dma16(ra, As + C::NW * j * 1024 + pad(j, KT::a_kc, MKP_A), va[j] + (KT::a_kc ? k0 * ES : k0 * a_ld));
     } else {
       const int j = idx - C::IA;
       if (KIND == BWD_DX) {
         const bool up = k0 >= f;
-        dma16(up ? rb1 : rb0, Bs + C::NW * j * 1024, vb[j] + (up ? k0 - f : k0) * b_ld);
+        dma16(up ? rb1 : rb0, Bs + C::NW * j * 1024 + pad(j, false, MKP_B), vb[j] + (up ? k0 - f : k0) * b_ld);
       } else {
-        dma16(bup[j] ? rb1 : rb0, Bs + C::NW * j * 1024 + (KT::b_kc ? pad(j) : 0),
+        dma16(bup[j] ? rb1 : rb0, Bs + C::NW * j * 1024 + pad(j, KT::b_kc, MKP_B),
               vb[j] + (KT::b_kc ? k0 * ES : k0 * b_ld));
       }
     }
@@ -295,10 +318,16 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
       // fragment i sits FRAG bytes after fragment 0 (an immediate offset of the LDS read)
       constexpr int FRAG = 16 * C::ROWB + 16;
       const int lane_kc = li * C::ROWB + (((4 * kk + q) ^ kc_swz<BK>(li)) << 4);
+      // padded K-major fragments: the lane's two k-rows (kl1, kl2) and its 8-byte column group
+      const int kl1 = 8 * q + 4 * (q & 1) + (li >> 2), kl2 = kl1 + 4 - 8 * (q & 1);
+      const int lane_mk = 16 * ((li & 3) >> 1) + 8 * (li & 1) + 16 * MK_BLOCK * kk;
+      const auto mk_lane = [&](int kl, int w) { return mk_row(kl) + 128 * ((w + (kl & 1)) & 3) + lane_mk; };
 #pragma unroll
       for (int i = 0; i < C::FM; ++i) {
         if (KT::a_kc) {
           a[i] = lds_kc_pair(As + kc_row<C::ROWB>(wm * C::WTM) + lane_kc + i * FRAG, q);
+        } else if (MKP_A) {
+          a[i] = lds_tr_pair(As + mk_lane(kl1, wm) + 32 * i, As + mk_lane(kl2, wm) + 32 * i);
         } else {
           const int k1 = 32 * kk + 8 * q + 4 * (q & 1) + (li >> 2), mn = wm * C::WTM + 16 * i + 4 * (li & 3);
           const int k2 = k1 + 4 - 8 * (q & 1);
@@ -310,6 +339,8 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
       for (int j = 0; j < C::FN; ++j) {
         if (KT::b_kc) {
           b[j] = lds_kc_pair(Bs + kc_row<C::ROWB>(wn * C::WTN) + lane_kc + j * FRAG, q);
+        } else if (MKP_B) {
+          b[j] = lds_tr_pair(Bs + mk_lane(kl1, wn) + 32 * j, Bs + mk_lane(kl2, wn) + 32 * j);
         } else {
           const int k1 = 32 * kk + 8 * q + 4 * (q & 1) + (li >> 2), mn = wn * C::WTN + 16 * j + 4 * (li & 3);
           const int k2 = k1 + 4 - 8 * (q & 1);
