@@ -11,7 +11,9 @@ static int token_blocks(int Tn) {
   return b > 8192 ? 8192 : (b < 1 ? 1 : b);
 }
 
-template <typename T>
+// Each lane handles CPL 16-byte chunks per pass; the chunks of all KM slots are loaded together (one round
+// trip per token for its map and weights, one for its rows).
+template <typename T, int KM, int CPL>
 __global__ __launch_bounds__(256) void combine_kernel(int Tn, int k, int S, int cpr, const Chunk* __restrict__ yp,
                                                       const int32_t* __restrict__ s2r,
                                                       const float* __restrict__ gw, Chunk* __restrict__ y) {
@@ -21,36 +23,48 @@ __global__ __launch_bounds__(256) void combine_kernel(int Tn, int k, int S, int 
   const int nwaves = (gridDim.x * blockDim.x) >> 6;
   const size_t shared_base = (size_t)Tn * k;
   for (int t = wave; t < Tn; t += nwaves) {
-    int rows[8];
-    float w[8];
+    int rows[KM];
+    float w[KM];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
+    for (int j = 0; j < KM; ++j) {
       rows[j] = (j < k) ? s2r[(size_t)t * k + j] : -1;
       w[j] = (j < k) ? gw[(size_t)t * k + j] : 0.f;
     }
-    for (int c = lane; c < cpr; c += 64) {
-      float acc[N], v[N];
+    for (int c0 = lane; c0 < cpr; c0 += 64 * CPL) {
+      Chunk in[KM][CPL];
 #pragma unroll
-      for (int i = 0; i < N; ++i) acc[i] = 0.f;
+      for (int j = 0; j < KM; ++j)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        if (rows[j] >= 0) {
-          chunk_to_f<T>(yp[(size_t)rows[j] * cpr + c], v);
+        for (int u = 0; u < CPL; ++u)
+          in[j][u] = (rows[j] >= 0 && c0 + 64 * u < cpr) ? yp[(size_t)rows[j] * cpr + c0 + 64 * u] : zero_chunk();
 #pragma unroll
-          for (int i = 0; i < N; ++i) acc[i] = fmaf(w[j], v[i], acc[i]);
+      for (int u = 0; u < CPL; ++u) {
+        const int c = c0 + 64 * u;
+        float acc[N], v[N];
+#pragma unroll
+        for (int i = 0; i < N; ++i) acc[i] = 0.f;
+#pragma unroll
+        for (int j = 0; j < KM; ++j) {
+          if (rows[j] >= 0) {
+            chunk_to_f<T>(in[j][u], v);
+#pragma unroll
+            for (int i = 0; i < N; ++i) acc[i] = fmaf(w[j], v[i], acc[i]);
+          }
+        }
+        if (c < cpr) {
+          for (int sh = 0; sh < S; ++sh) {
+            chunk_to_f<T>(yp[(shared_base + (size_t)sh * Tn + t) * cpr + c], v);
+#pragma unroll
+            for (int i = 0; i < N; ++i) acc[i] += v[i];
+          }
+          y[(size_t)t * cpr + c] = f_to_chunk<T>(acc);
         }
       }
-      for (int sh = 0; sh < S; ++sh) {
-        chunk_to_f<T>(yp[(shared_base + (size_t)sh * Tn + t) * cpr + c], v);
-#pragma unroll
-        for (int i = 0; i < N; ++i) acc[i] += v[i];
-      }
-      y[(size_t)t * cpr + c] = f_to_chunk<T>(acc);
     }
   }
 }
 
-template <typename T>
+template <typename T, int KM, int CPL>
 __global__ __launch_bounds__(256) void combine_bwd_kernel(int Tn, int k, int cpr, const Chunk* __restrict__ dy,
                                                           const Chunk* __restrict__ yp,
                                                           const int32_t* __restrict__ s2r,
@@ -61,32 +75,44 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(int Tn, int k, int cpr
   const int wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int nwaves = (gridDim.x * blockDim.x) >> 6;
   for (int t = wave; t < Tn; t += nwaves) {
-    int rows[8];
-    float w[8], dot[8];
+    int rows[KM];
+    float w[KM], dot[KM];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
+    for (int j = 0; j < KM; ++j) {
       rows[j] = (j < k) ? s2r[(size_t)t * k + j] : -1;
       w[j] = (j < k) ? gw[(size_t)t * k + j] : 0.f;
       dot[j] = 0.f;
     }
-    for (int c = lane; c < cpr; c += 64) {
-      float g[N], o[N], s[N];
-      chunk_to_f<T>(dy[(size_t)t * cpr + c], g);
+    for (int c0 = lane; c0 < cpr; c0 += 64 * CPL) {
+      Chunk gc[CPL], in[KM][CPL];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        if (rows[j] >= 0) {
-          chunk_to_f<T>(yp[(size_t)rows[j] * cpr + c], o);
+      for (int u = 0; u < CPL; ++u) gc[u] = (c0 + 64 * u < cpr) ? dy[(size_t)t * cpr + c0 + 64 * u] : zero_chunk();
 #pragma unroll
-          for (int i = 0; i < N; ++i) {
-            dot[j] = fmaf(g[i], o[i], dot[j]);
-            s[i] = w[j] * g[i];
+      for (int j = 0; j < KM; ++j)
+#pragma unroll
+        for (int u = 0; u < CPL; ++u)
+          in[j][u] = (rows[j] >= 0 && c0 + 64 * u < cpr) ? yp[(size_t)rows[j] * cpr + c0 + 64 * u] : zero_chunk();
+#pragma unroll
+      for (int u = 0; u < CPL; ++u) {
+        const int c = c0 + 64 * u;
+        float g[N], o[N], sc[N];
+        chunk_to_f<T>(gc[u], g);
+#pragma unroll
+        for (int j = 0; j < KM; ++j) {
+          if (rows[j] >= 0 && c < cpr) {
+            chunk_to_f<T>(in[j][u], o);
+#pragma unroll
+            for (int i = 0; i < N; ++i) {
+              dot[j] = fmaf(g[i], o[i], dot[j]);
+              sc[i] = w[j] * g[i];
+            }
+            dyp[(size_t)rows[j] * cpr + c] = f_to_chunk<T>(sc);
           }
-          dyp[(size_t)rows[j] * cpr + c] = f_to_chunk<T>(s);
         }
       }
     }
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
+    for (int j = 0; j < KM; ++j) {
       if (j < k) {
         float tot = wave_sum(dot[j]);
         if (lane == 0) dgate[(size_t)t * k + j] = (rows[j] >= 0) ? tot : 0.f;
@@ -99,12 +125,15 @@ hipError_t launch_combine(const moe_desc& d, const void* yp, const int32_t* s2r,
                           hipStream_t s) {
   const int cpr = (int)(d.d_model * elem_bytes(d) / 16);
   KernelTimer kt("combine", s);
-  if (d.dtype == MOE_BF16)
-    hipLaunchKernelGGL(combine_kernel<bf16>, dim3(token_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k, d.n_shared,
-                       cpr, (const Chunk*)yp, s2r, w, (Chunk*)y);
-  else
-    hipLaunchKernelGGL(combine_kernel<float>, dim3(token_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k, d.n_shared,
-                       cpr, (const Chunk*)yp, s2r, w, (Chunk*)y);
+  row_dispatch(d.top_k, cpr, [&](auto km, auto cpl) {
+    constexpr int KM = decltype(km)::value, CPL = decltype(cpl)::value;
+    if (d.dtype == MOE_BF16)
+      hipLaunchKernelGGL((combine_kernel<bf16, KM, CPL>), dim3(token_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k,
+                         d.n_shared, cpr, (const Chunk*)yp, s2r, w, (Chunk*)y);
+    else
+      hipLaunchKernelGGL((combine_kernel<float, KM, CPL>), dim3(token_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k,
+                         d.n_shared, cpr, (const Chunk*)yp, s2r, w, (Chunk*)y);
+  });
   return hipGetLastError();
 }
 
@@ -112,12 +141,15 @@ hipError_t launch_combine_bwd(const moe_desc& d, const void* dy, const void* yp,
                               const float* w, void* dyp, float* dgate, hipStream_t s) {
   const int cpr = (int)(d.d_model * elem_bytes(d) / 16);
   KernelTimer kt("combine_bwd", s);
-  if (d.dtype == MOE_BF16)
-    hipLaunchKernelGGL(combine_bwd_kernel<bf16>, dim3(token_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k, cpr,
-                       (const Chunk*)dy, (const Chunk*)yp, s2r, w, (Chunk*)dyp, dgate);
-  else
-    hipLaunchKernelGGL(combine_bwd_kernel<float>, dim3(token_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k, cpr,
-                       (const Chunk*)dy, (const Chunk*)yp, s2r, w, (Chunk*)dyp, dgate);
+  row_dispatch(d.top_k, cpr, [&](auto km, auto cpl) {
+    constexpr int KM = decltype(km)::value, CPL = decltype(cpl)::value;
+    if (d.dtype == MOE_BF16)
+      hipLaunchKernelGGL((combine_bwd_kernel<bf16, KM, CPL>), dim3(token_blocks(d.T)), dim3(256), 0, s, d.T,
+                         d.top_k, cpr, (const Chunk*)dy, (const Chunk*)yp, s2r, w, (Chunk*)dyp, dgate);
+    else
+      hipLaunchKernelGGL((combine_bwd_kernel<float, KM, CPL>), dim3(token_blocks(d.T)), dim3(256), 0, s, d.T,
+                         d.top_k, cpr, (const Chunk*)dy, (const Chunk*)yp, s2r, w, (Chunk*)dyp, dgate);
+  });
   return hipGetLastError();
 }
 

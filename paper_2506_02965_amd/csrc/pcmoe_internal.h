@@ -1,5 +1,6 @@
 // Private helpers of the pcmoe HIP library (gfx950 / CDNA4). Not part of the ABI.
 #pragma once
+#include <type_traits>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 #include <stddef.h>
@@ -88,6 +89,22 @@ __device__ __forceinline__ float wave_max(float v) {
 }
 
 // ---------------------------------------------------------------- host side
+
+// Per-token row kernels are instantiated for KM = top_k rounded up to 1, 2, 4 or 8 and CPL = 16-byte chunks
+// per lane per pass (1, 2 or 4: a row of cpr chunks takes ceil(cpr / (64 CPL)) passes). f(km, cpl) receives
+// both as std::integral_constant.
+template <typename F>
+inline void row_dispatch(int k, int cpr, F&& f) {
+  auto with_km = [&](auto km) {
+    if (cpr <= 64) f(km, std::integral_constant<int, 1>{});
+    else if (cpr <= 128) f(km, std::integral_constant<int, 2>{});
+    else f(km, std::integral_constant<int, 4>{});
+  };
+  if (k <= 1) with_km(std::integral_constant<int, 1>{});
+  else if (k <= 2) with_km(std::integral_constant<int, 2>{});
+  else if (k <= 4) with_km(std::integral_constant<int, 4>{});
+  else with_km(std::integral_constant<int, 8>{});
+}
 
 // Bracket a kernel launch with HIP events when per-kernel timing is on (no-op otherwise).
 struct KernelTimer {

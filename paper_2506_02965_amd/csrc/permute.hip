@@ -134,20 +134,31 @@ __global__ __launch_bounds__(256) void perm_scatter_kernel(const int32_t* __rest
 }
 
 // Token-major gather: x_perm[slot_to_row[t*k+j]] = x[t] for every hosted slot.
+// One wavefront per token. Each lane handles CPL 16-byte chunks of the row per pass, loaded together, so a
+// token costs one round trip for its slot map and its row, not one per chunk.
+template <int KM, int CPL>
 __global__ __launch_bounds__(256) void perm_gather_kernel(int Tn, int k, int cpr, const Chunk* __restrict__ x,
                                                           const int32_t* __restrict__ s2r, Chunk* __restrict__ xp) {
   const int lane = threadIdx.x & 63;
   const int wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int nwaves = (gridDim.x * blockDim.x) >> 6;
   for (int t = wave; t < Tn; t += nwaves) {
-    int rows[8];
+    int rows[KM];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) rows[j] = (j < k) ? s2r[(size_t)t * k + j] : -1;
-    for (int c = lane; c < cpr; c += 64) {
-      const Chunk v = x[(size_t)t * cpr + c];
+    for (int j = 0; j < KM; ++j) rows[j] = (j < k) ? s2r[(size_t)t * k + j] : -1;
+    for (int c0 = lane; c0 < cpr; c0 += 64 * CPL) {
+      Chunk v[CPL];
 #pragma unroll
-      for (int j = 0; j < 8; ++j)
-        if (rows[j] >= 0) xp[(size_t)rows[j] * cpr + c] = v;
+      for (int u = 0; u < CPL; ++u) v[u] = (c0 + 64 * u < cpr) ? x[(size_t)t * cpr + c0 + 64 * u] : zero_chunk();
+#pragma unroll
+      for (int u = 0; u < CPL; ++u) {
+        const int c = c0 + 64 * u;
+        if (c < cpr) {
+#pragma unroll
+          for (int j = 0; j < KM; ++j)
+            if (rows[j] >= 0) xp[(size_t)rows[j] * cpr + c] = v[u];
+        }
+      }
     }
   }
 }
@@ -188,16 +199,20 @@ hipError_t launch_permute(const moe_desc& d, const int32_t* idx, const void* x, 
   {
     KernelTimer kt("permute_gather", s);
     const int cpr = (int)(d.d_model * elem_bytes(d) / 16);
-    hipLaunchKernelGGL(perm_gather_kernel, dim3(gather_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k, cpr,
-                       (const Chunk*)x, s2r, (Chunk*)xp);
+    row_dispatch(d.top_k, cpr, [&](auto km, auto cpl) {
+      hipLaunchKernelGGL((perm_gather_kernel<decltype(km)::value, decltype(cpl)::value>), dim3(gather_blocks(d.T)),
+                         dim3(256), 0, s, d.T, d.top_k, cpr, (const Chunk*)x, s2r, (Chunk*)xp);
+    });
   }
   return hipGetLastError();
 }
 
 // dx_t = sum_j dx_perm[row(t,j)] + sum_s dx_perm[T*k + s*T + t] (+ sum_e dlogits[t,e] * w_router[e])
-// One wavefront per token. The token's dlogits row is read once; its nonzero experts (k of them when
-// the gate weights are renormalised) are found with ballots and only their router rows are read.
-template <typename T>
+// One wavefront per token. The token's dlogits row is read once, together with its slot map; its nonzero
+// experts (k of them when the gate weights are renormalised) are found with ballots and only their router
+// rows are read, four experts' chunks at a time. Each lane handles CPL chunks of the row per pass; the
+// sums run in slot order, then shared experts, then experts in increasing index.
+template <typename T, int KM, int CPL>
 __global__ __launch_bounds__(256) void unpermute_kernel(int Tn, int k, int S, int E, int cpr,
                                                         const Chunk* __restrict__ dxp,
                                                         const int32_t* __restrict__ s2r,
@@ -209,9 +224,9 @@ __global__ __launch_bounds__(256) void unpermute_kernel(int Tn, int k, int S, in
   const int nwaves = (gridDim.x * blockDim.x) >> 6;
   const size_t shared_base = (size_t)Tn * k;
   for (int t = wave; t < Tn; t += nwaves) {
-    int rows[8];
+    int rows[KM];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) rows[j] = (j < k) ? s2r[(size_t)t * k + j] : -1;
+    for (int j = 0; j < KM; ++j) rows[j] = (j < k) ? s2r[(size_t)t * k + j] : -1;
     float g[4] = {0.f, 0.f, 0.f, 0.f};
     uint64_t nz[4] = {0ull, 0ull, 0ull, 0ull};
     if (dl) {
@@ -219,40 +234,80 @@ __global__ __launch_bounds__(256) void unpermute_kernel(int Tn, int k, int S, in
       for (int qq = 0; qq < 4; ++qq) {
         const int e = lane + 64 * qq;
         g[qq] = (e < E) ? dl[(size_t)t * E + e] : 0.f;
-        nz[qq] = __ballot(g[qq] != 0.f);
       }
+#pragma unroll
+      for (int qq = 0; qq < 4; ++qq) nz[qq] = __ballot(g[qq] != 0.f);
     }
-    for (int c = lane; c < cpr; c += 64) {
-      float acc[N];
+    for (int c0 = lane; c0 < cpr; c0 += 64 * CPL) {
+      Chunk in[KM][CPL];
 #pragma unroll
-      for (int i = 0; i < N; ++i) acc[i] = 0.f;
-      float v[N];
+      for (int j = 0; j < KM; ++j)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        if (rows[j] >= 0) {
-          chunk_to_f<T>(dxp[(size_t)rows[j] * cpr + c], v);
+        for (int u = 0; u < CPL; ++u)
+          in[j][u] = (rows[j] >= 0 && c0 + 64 * u < cpr) ? dxp[(size_t)rows[j] * cpr + c0 + 64 * u] : zero_chunk();
+      float acc[CPL][N], v[N];
 #pragma unroll
-          for (int i = 0; i < N; ++i) acc[i] += v[i];
+      for (int u = 0; u < CPL; ++u) {
+#pragma unroll
+        for (int i = 0; i < N; ++i) acc[u][i] = 0.f;
+#pragma unroll
+        for (int j = 0; j < KM; ++j) {
+          if (rows[j] >= 0) {
+            chunk_to_f<T>(in[j][u], v);
+#pragma unroll
+            for (int i = 0; i < N; ++i) acc[u][i] += v[i];
+          }
         }
       }
       for (int sh = 0; sh < S; ++sh) {
-        chunk_to_f<T>(dxp[(shared_base + (size_t)sh * Tn + t) * cpr + c], v);
 #pragma unroll
-        for (int i = 0; i < N; ++i) acc[i] += v[i];
+        for (int u = 0; u < CPL; ++u) {
+          if (c0 + 64 * u < cpr) {
+            chunk_to_f<T>(dxp[(shared_base + (size_t)sh * Tn + t) * cpr + c0 + 64 * u], v);
+#pragma unroll
+            for (int i = 0; i < N; ++i) acc[u][i] += v[i];
+          }
+        }
       }
 #pragma unroll
       for (int qq = 0; qq < 4; ++qq) {
         uint64_t m = nz[qq];
-        while (m) {  // wave-uniform loop over the nonzero experts, in increasing order
-          const int e = __builtin_ctzll(m) + 64 * qq;
-          m &= m - 1;
-          const float ge = dl[(size_t)t * E + e];  // same address in every lane (lanes past cpr are idle here)
-          chunk_to_f<T>(wr[(size_t)e * cpr + c], v);
+        while (m) {  // wave-uniform: up to four nonzero experts per round, in increasing order
+          int es[4];
+          float ge[4];
 #pragma unroll
-          for (int i = 0; i < N; ++i) acc[i] = fmaf(ge, v[i], acc[i]);
+          for (int b = 0; b < 4; ++b) {
+            es[b] = -1;
+            ge[b] = 0.f;
+            if (m) {
+              const int l = __builtin_ctzll(m);
+              m &= m - 1;
+              es[b] = l + 64 * qq;
+              ge[b] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(g[qq]), l));
+            }
+          }
+          Chunk wv[4][CPL];
+#pragma unroll
+          for (int b = 0; b < 4; ++b)
+#pragma unroll
+            for (int u = 0; u < CPL; ++u)
+              wv[b][u] = (es[b] >= 0 && c0 + 64 * u < cpr) ? wr[(size_t)es[b] * cpr + c0 + 64 * u] : zero_chunk();
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            if (es[b] >= 0) {
+#pragma unroll
+              for (int u = 0; u < CPL; ++u) {
+                chunk_to_f<T>(wv[b][u], v);
+#pragma unroll
+                for (int i = 0; i < N; ++i) acc[u][i] = fmaf(ge[b], v[i], acc[u][i]);
+              }
+            }
+          }
         }
       }
-      dx[(size_t)t * cpr + c] = f_to_chunk<T>(acc);
+#pragma unroll
+      for (int u = 0; u < CPL; ++u)
+        if (c0 + 64 * u < cpr) dx[(size_t)t * cpr + c0 + 64 * u] = f_to_chunk<T>(acc[u]);
     }
   }
 }
@@ -261,12 +316,15 @@ hipError_t launch_permute_bwd(const moe_desc& d, const void* dxp, const int32_t*
                               const void* wr, void* dx, hipStream_t s) {
   const int cpr = (int)(d.d_model * elem_bytes(d) / 16);
   KernelTimer kt("unpermute", s);
-  if (d.dtype == MOE_BF16)
-    hipLaunchKernelGGL(unpermute_kernel<bf16>, dim3(gather_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k, d.n_shared,
-                       d.n_experts, cpr, (const Chunk*)dxp, s2r, dl, (const Chunk*)wr, (Chunk*)dx);
-  else
-    hipLaunchKernelGGL(unpermute_kernel<float>, dim3(gather_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k,
-                       d.n_shared, d.n_experts, cpr, (const Chunk*)dxp, s2r, dl, (const Chunk*)wr, (Chunk*)dx);
+  row_dispatch(d.top_k, cpr, [&](auto km, auto cpl) {
+    constexpr int KM = decltype(km)::value, CPL = decltype(cpl)::value;
+    if (d.dtype == MOE_BF16)
+      hipLaunchKernelGGL((unpermute_kernel<bf16, KM, CPL>), dim3(gather_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k,
+                         d.n_shared, d.n_experts, cpr, (const Chunk*)dxp, s2r, dl, (const Chunk*)wr, (Chunk*)dx);
+    else
+      hipLaunchKernelGGL((unpermute_kernel<float, KM, CPL>), dim3(gather_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k,
+                         d.n_shared, d.n_experts, cpr, (const Chunk*)dxp, s2r, dl, (const Chunk*)wr, (Chunk*)dx);
+  });
   return hipGetLastError();
 }
 
