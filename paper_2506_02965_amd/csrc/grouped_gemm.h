@@ -10,7 +10,8 @@ struct GemmArgs {
   int T, k, d, f, Eloc, S;
   int rows_cap;               // T*k: first row of the shared experts in the row space
   const int32_t* offsets;     // [Eloc+1]
-  const int32_t* mt_prefix;   // [G+1] m-tile prefix of the row-ragged kinds
+  const int32_t* mt_prefix;   // [G+1] m-tile prefix of the row-ragged kinds (without the tails when mt_tail is set)
+  const int32_t* mt_tail;     // [G+1] prefix of the groups' tail m-tiles (at most half their rows), or null
   const int32_t* order;       // [G] groups by decreasing row count (weight-gradient kinds), or null
   int n_tiles, m_tiles;       // tiles along N (all kinds) and along M (weight-gradient kinds)
   const void* x;              // [T, d]
@@ -63,15 +64,18 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs& p, int bid, TileIdx&
   const int ns = (G + 64) >> 6;  // slots covering entries 0..G
   // One batch of independent loads (a chain of dependent ones costs a memory latency each): the
   // m-tile prefix (ragged kinds), the group order (weight gradients) and the row offsets.
-  int pre[NS], ord[NS], off[NS];
+  int pre[NS], ord[NS], off[NS], tl[NS];
+  const bool split = RAGGED && p.mt_tail != nullptr;
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
     const int i = 64 * s + lane;
     pre[s] = 0;
     ord[s] = 0;
     off[s] = 0;
+    tl[s] = 0;
     if (s < ns) {
       if (RAGGED && i <= G) pre[s] = p.mt_prefix[i];
+      if (split && i <= G) tl[s] = p.mt_tail[i];
       if (!RAGGED && p.order && i < G) ord[s] = p.order[i];
       if (i <= p.Eloc) off[s] = p.offsets[i];
     }
@@ -80,18 +84,54 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs& p, int bid, TileIdx&
   if (RAGGED) total = wave_pick(pre, G) * p.n_tiles;
   else total = G * p.m_tiles * p.n_tiles;
   // Ragged kinds: equal-cost tiles, so each XCD takes a contiguous run of them (its L2 then holds the
-  // weights of few groups). Weight-gradient tiles cost K = rows of their group, heaviest groups
-  // first; they are dealt round-robin over the XCDs so that the long ones spread out.
+  // weights of few groups). With mt_tail, a group's last m-tile holding at most half a tile of rows (its
+  // empty wavefronts skip their MFMAs) is left out of that run: each XCD takes its share of those cheap
+  // tiles after its share of the others, so that they fill the last, partial round of tiles. Weight-gradient
+  // tiles cost K = rows of their group, heaviest groups first; they are dealt round-robin over the XCDs so
+  // that the long ones spread out.
   int L;
+  bool tail = false;
   if (RAGGED) {
     const int per_xcd = (total + 7) >> 3;
-    if ((bid >> 3) >= per_xcd) return false;
-    L = (bid & 7) * per_xcd + (bid >> 3);
+    const int lb = bid >> 3;
+    if (lb < per_xcd) {
+      L = (bid & 7) * per_xcd + lb;
+    } else {
+      if (!split) return false;
+      const int ptot = wave_pick(tl, G) * p.n_tiles;
+      const int per_xcd_t = (ptot + 7) >> 3;
+      const int lt = lb - per_xcd;
+      if (lt >= per_xcd_t) return false;
+      L = (bid & 7) * per_xcd_t + lt;
+      if (L >= ptot) return false;
+      tail = true;
+    }
   } else {
     L = bid;
   }
-  if (L >= total) return false;
+  if (!tail && L >= total) return false;
   int l, n_mt;
+  if (tail) {
+    // the group of tail tile L / n_tiles: largest g whose tail prefix is <= it (groups without a tail share
+    // their successor's prefix and are passed over)
+    const int tix = L / p.n_tiles;
+    int g = 0;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      if (s < ns) {
+        const int i = 64 * s + lane;
+        g += __popcll(__ballot(i >= 1 && i < G && tl[s] <= tix));
+      }
+    }
+    g = __builtin_amdgcn_readfirstlane(g);
+    t.g = g;
+    const bool routed_t = g < p.Eloc;
+    t.row0 = routed_t ? wave_pick(off, g) : 0;
+    t.rows = routed_t ? wave_pick(off, g + 1) - t.row0 : p.T;
+    t.nt = __builtin_amdgcn_readfirstlane(L - tix * p.n_tiles);
+    t.mt = __builtin_amdgcn_readfirstlane(wave_pick(pre, g + 1) - wave_pick(pre, g));  // after the group's others
+    return true;
+  }
   if (RAGGED) {
     // largest g < G with pre[g] * n_tiles <= L (pre is non-decreasing from pre[0] = 0)
     int g = 0;
@@ -124,9 +164,14 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs& p, int bid, TileIdx&
   return true;
 }
 
+// Tile plan of the row-ragged contractions (one workgroup of 512 threads: at most 511 groups): pre0 = m-tile
+// prefix for bm0-row tiles; for bm1-row tiles pre1 = prefix of the m-tiles other than the tails and tail1 =
+// prefix of the tails (a last m-tile holding at most bm1 / 2 rows); order = groups by decreasing row count
+// (ties by index).
 __global__ __launch_bounds__(512) void mtile_prefix_kernel(const int32_t* __restrict__ offsets, int Eloc, int S,
                                                            int Tn, int bm0, int bm1, int32_t* __restrict__ pre0,
-                                                           int32_t* __restrict__ pre1, int32_t* __restrict__ order);
+                                                           int32_t* __restrict__ pre1, int32_t* __restrict__ tail1,
+                                                           int32_t* __restrict__ order);
 
 // fp32 path (generic LDS-tiled MFMA 16x16x4 kernel)
 hipError_t ffn_fwd_f32(const moe_desc& d, const void* x, const void* xp, const int32_t* offsets, const void* wg,

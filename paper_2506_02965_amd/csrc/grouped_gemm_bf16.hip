@@ -272,6 +272,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
     };
     if (idx < C::IA) {
       const int j = idx;
+      // Row-ragged tiles: an instruction whose rows all lie past the group's end is skipped (two-stage ring,
+      // where the waits are vmcnt(0)); those rows' outputs are never stored, and no other row reads them.
+      if (KT::ragged_m && STAGES == 2 && m0 + C::RPI * (wave + C::NW * j) >= rows) return;
       dma16(ra, As + C::NW * j * 1024 + pad(j, KT::a_kc, MKP_A), va[j] + (KT::a_kc ? k0 * ES : k0 * a_ld));
     } else {
       const int j = idx - C::IA;
@@ -302,6 +305,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
     if (s < KTN) issue(s, s);
 
   const int q = lane >> 4, li = lane & 15;
+  const bool wave_rows = !KT::ragged_m || m0 + wm * C::WTM < rows;  // wave-uniform
   for (int kt = 0; kt < KTN; ++kt) {
     // tile kt has landed when at most the later tiles' loads are outstanding
     if (kt + STAGES - 2 < KTN) wait_vmcnt<(STAGES - 2) * C::LOADS>();
@@ -309,6 +313,8 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
     // every wave's loads of tile kt have landed and its reads of the stage about to be refilled are done
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     if (kt + STAGES - 1 < KTN) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
+    // a wavefront whose rows all lie past the group's end has nothing to compute (it still loads and syncs)
+    if (!wave_rows) continue;
     const char* As = smem + (kt % STAGES) * C::STAGE_BYTES;
     const char* Bs = As + C::A_BYTES;
 #pragma unroll
@@ -563,7 +569,7 @@ static long mtile_bound2(const moe_desc& d, int bm) {
 }
 
 static size_t plan_part(const moe_desc& d) { return align256((size_t)(d.local_count + d.n_shared + 1) * 4); }
-static size_t plan_bytes(const moe_desc& d) { return 3 * plan_part(d); }
+static size_t plan_bytes(const moe_desc& d) { return 4 * plan_part(d); }
 // saved = G|U [R, 2f], H [R, f], then the tile plan of the forward, which the backward reuses
 static size_t saved_plan_offset(const moe_desc& d) {
   const size_t R = (size_t)rows_total(d), es = elem_bytes(d);
@@ -578,23 +584,26 @@ size_t ffn_bwd_ws_bytes(const moe_desc& d) {
 
 struct Plan {
   int32_t* pre128;
-  int32_t* pre256;
+  int32_t* pre256;   // 256-row m-tiles other than the tails
   int32_t* order;
+  int32_t* tail256;  // 256-row tail m-tiles (at most 128 rows)
 };
 
-// The plan's arrays at `where`: m-tile prefixes for 128- and 256-row tiles and the heaviest-first group order.
+// The plan's arrays at `where`: m-tile prefixes for 128-row tiles and for 256-row tiles (tails apart), and the
+// heaviest-first group order.
 static Plan plan_at(const moe_desc& d, void* where) {
   Plan pl;
   pl.pre128 = (int32_t*)where;
   pl.pre256 = (int32_t*)((char*)where + plan_part(d));
   pl.order = (int32_t*)((char*)where + 2 * plan_part(d));
+  pl.tail256 = (int32_t*)((char*)where + 3 * plan_part(d));
   return pl;
 }
 static Plan plan(const moe_desc& d, const int32_t* offsets, void* where, hipStream_t s) {
   Plan pl = plan_at(d, where);
   KernelTimer kt("ffn_plan", s);
   hipLaunchKernelGGL(mtile_prefix_kernel, dim3(1), dim3(512), 0, s, offsets, d.local_count, d.n_shared, d.T, 128, 256,
-                     pl.pre128, pl.pre256, pl.order);
+                     pl.pre128, pl.pre256, pl.tail256, pl.order);
   return pl;
 }
 
@@ -604,6 +613,18 @@ static GemmArgs args_for(const moe_desc& d, const int32_t* offsets) {
   a.rows_cap = d.T * d.top_k;
   a.offsets = offsets;
   return a;
+}
+
+// Compute units of the current device (queried once per device).
+static int device_cus() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] <= 0) {
+    int n = 0;
+    cus[dev] = (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0) ? n : 256;
+  }
+  return cus[dev];
 }
 
 // Ragged-M contraction: n_cols output columns of the tile grid (FWD_GU: gate columns, two per pair).
@@ -635,7 +656,12 @@ static Prep prep_ragged(const moe_desc& d, GemmArgs a, const Plan& pl, int n_col
   const int bm = kShapeBM[sh], bn = kShapeBN[sh];
   a.mt_prefix = bm == 128 ? pl.pre128 : pl.pre256;
   a.n_tiles = n_cols / bn;  // FWD_GU: n_cols = 2f, each tile holds bn/2 gate and bn/2 up columns
-  return Prep{sh, a, mtile_bound2(d, bm) * a.n_tiles};
+  const long bound = mtile_bound2(d, bm) * a.n_tiles;
+  // 256-row tiles in more than one round of the chip: tails after the others (see decode_tile); each XCD
+  // rounds its share of both segments up, at most 16 workgroups more
+  const bool split = bm == 256 && bound > device_cus();
+  a.mt_tail = split ? pl.tail256 : nullptr;
+  return Prep{sh, a, bound + (split ? 16 : 0)};
 }
 // Weight gradient: an M x N output per group, K = the group's rows.
 template <int KIND>
