@@ -569,7 +569,7 @@ static long mtile_bound2(const moe_desc& d, int bm) {
 }
 
 static size_t plan_part(const moe_desc& d) { return align256((size_t)(d.local_count + d.n_shared + 1) * 4); }
-static size_t plan_bytes(const moe_desc& d) { return 4 * plan_part(d); }
+static size_t plan_bytes(const moe_desc& d) { return 5 * plan_part(d); }
 // saved = G|U [R, 2f], H [R, f], then the tile plan of the forward, which the backward reuses
 static size_t saved_plan_offset(const moe_desc& d) {
   const size_t R = (size_t)rows_total(d), es = elem_bytes(d);
@@ -584,26 +584,28 @@ size_t ffn_bwd_ws_bytes(const moe_desc& d) {
 
 struct Plan {
   int32_t* pre128;
-  int32_t* pre256;   // 256-row m-tiles other than the tails
+  int32_t* pre256;
   int32_t* order;
+  int32_t* body256;  // 256-row m-tiles other than the tails
   int32_t* tail256;  // 256-row tail m-tiles (at most 128 rows)
 };
 
-// The plan's arrays at `where`: m-tile prefixes for 128-row tiles and for 256-row tiles (tails apart), and the
-// heaviest-first group order.
+// The plan's arrays at `where`: m-tile prefixes for 128- and 256-row tiles, the heaviest-first group order, and
+// for 256-row tiles the prefixes without the tails and of the tails.
 static Plan plan_at(const moe_desc& d, void* where) {
   Plan pl;
   pl.pre128 = (int32_t*)where;
   pl.pre256 = (int32_t*)((char*)where + plan_part(d));
   pl.order = (int32_t*)((char*)where + 2 * plan_part(d));
-  pl.tail256 = (int32_t*)((char*)where + 3 * plan_part(d));
+  pl.body256 = (int32_t*)((char*)where + 3 * plan_part(d));
+  pl.tail256 = (int32_t*)((char*)where + 4 * plan_part(d));
   return pl;
 }
 static Plan plan(const moe_desc& d, const int32_t* offsets, void* where, hipStream_t s) {
   Plan pl = plan_at(d, where);
   KernelTimer kt("ffn_plan", s);
   hipLaunchKernelGGL(mtile_prefix_kernel, dim3(1), dim3(512), 0, s, offsets, d.local_count, d.n_shared, d.T, 128, 256,
-                     pl.pre128, pl.pre256, pl.tail256, pl.order);
+                     pl.pre128, pl.pre256, pl.body256, pl.tail256, pl.order);
   return pl;
 }
 
@@ -654,12 +656,12 @@ template <int KIND>
 static Prep prep_ragged(const moe_desc& d, GemmArgs a, const Plan& pl, int n_cols) {
   const int sh = fit_shape(tile_shape(KIND, d), 0, n_cols);
   const int bm = kShapeBM[sh], bn = kShapeBN[sh];
-  a.mt_prefix = bm == 128 ? pl.pre128 : pl.pre256;
   a.n_tiles = n_cols / bn;  // FWD_GU: n_cols = 2f, each tile holds bn/2 gate and bn/2 up columns
   const long bound = mtile_bound2(d, bm) * a.n_tiles;
   // 256-row tiles in more than one round of the chip: tails after the others (see decode_tile); each XCD
   // rounds its share of both segments up, at most 16 workgroups more
   const bool split = bm == 256 && bound > device_cus();
+  a.mt_prefix = bm == 128 ? pl.pre128 : split ? pl.body256 : pl.pre256;
   a.mt_tail = split ? pl.tail256 : nullptr;
   return Prep{sh, a, bound + (split ? 16 : 0)};
 }

@@ -361,9 +361,9 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(GemmArgs p) 
 // the groups ordered by decreasing row count (ties by index).
 __global__ __launch_bounds__(512) void mtile_prefix_kernel(const int32_t* __restrict__ offsets, int Eloc, int S,
                                                            int Tn, int bm0, int bm1, int32_t* __restrict__ pre0,
-                                                           int32_t* __restrict__ pre1, int32_t* __restrict__ tail1,
-                                                           int32_t* __restrict__ order) {
-  __shared__ int buf[3][2][512];
+                                                           int32_t* __restrict__ pre1, int32_t* __restrict__ body1,
+                                                           int32_t* __restrict__ tail1, int32_t* __restrict__ order) {
+  __shared__ int buf[4][2][512];
   __shared__ int rows_s[512];
   const int g = threadIdx.x;
   const int G = Eloc + S;
@@ -373,8 +373,9 @@ __global__ __launch_bounds__(512) void mtile_prefix_kernel(const int32_t* __rest
   // bm1 tiles: a last m-tile with at most half its rows is a tail, counted apart
   const int rem1 = rows % bm1, is_tail = (rem1 > 0 && 2 * rem1 <= bm1) ? 1 : 0;
   buf[0][0][g] = (rows + bm0 - 1) / bm0;
-  buf[1][0][g] = (rows + bm1 - 1) / bm1 - is_tail;
-  buf[2][0][g] = is_tail;
+  buf[1][0][g] = (rows + bm1 - 1) / bm1;
+  buf[2][0][g] = (rows + bm1 - 1) / bm1 - is_tail;
+  buf[3][0][g] = is_tail;
   rows_s[g] = rows;
   __syncthreads();
   if (g < G) {
@@ -385,7 +386,7 @@ __global__ __launch_bounds__(512) void mtile_prefix_kernel(const int32_t* __rest
   int cur = 0;
   for (int off = 1; off < 512; off <<= 1) {
 #pragma unroll
-    for (int w = 0; w < 3; ++w) {
+    for (int w = 0; w < 4; ++w) {
       int x = buf[w][cur][g];
       if (g >= off) x += buf[w][cur][g - off];
       buf[w][cur ^ 1][g] = x;
@@ -396,7 +397,8 @@ __global__ __launch_bounds__(512) void mtile_prefix_kernel(const int32_t* __rest
   if (g <= G) {
     pre0[g] = (g == 0) ? 0 : buf[0][cur][g - 1];
     pre1[g] = (g == 0) ? 0 : buf[1][cur][g - 1];
-    tail1[g] = (g == 0) ? 0 : buf[2][cur][g - 1];
+    body1[g] = (g == 0) ? 0 : buf[2][cur][g - 1];
+    tail1[g] = (g == 0) ? 0 : buf[3][cur][g - 1];
   }
 }
 

@@ -50,6 +50,22 @@ def small_cases():
     C["all_tokens_one_expert"] = (LayerConfig("a1", T=384, d=128, f=256, E=4, k=1, bias="forced_empty", seed=20),
                                   all_to_one)
 
+    # Expert row counts set through a per-token logit bias: remainders 0, 1, 64, 65, 128, 129 and 255 of the
+    # 256-row m-tiles, an empty expert, and more 256 x 256 tiles than CUs in the gate/up contraction
+    # (tail m-tiles of at most 128 rows scheduled after the others).
+    tail_counts = [0, 1, 320, 321, 384, 385, 511, 1174, 1000]
+
+    def forced_counts(inp):
+        T = inp.cfg.T
+        slots = np.repeat(np.arange(len(tail_counts)), tail_counts)  # 2T slots, sorted by expert
+        assert slots.size == 2 * T
+        inp.logit_bias[:] = -1e4
+        t = np.arange(T)
+        inp.logit_bias[t, slots[:T]] = 2e4  # first choice
+        inp.logit_bias[t, slots[T:]] = 1e4  # second choice: another expert (no count exceeds T)
+    C["tail_tiles_forced_counts"] = (LayerConfig("tt", T=2048, d=256, f=2048, E=len(tail_counts), k=2, bias="party",
+                                                 parties=2048, seed=26), forced_counts)
+
     def zero_router(inp):
         inp.w_router[:] = 0
     C["ties_all_equal"] = (LayerConfig("z", T=256, d=128, f=128, E=8, k=3, seed=21), zero_router)
