@@ -142,6 +142,35 @@ def measure_expert_update(P, layer, w, steps):
                          "frac": round(gbs / HBM_PEAK_GBS, 4)}}
 
 
+def hbm_steps(cfg, n_routed, kernels):
+    """Achieved HBM bandwidth of the bandwidth-bound steps from their algorithmic bytes per launch
+    (s = element bytes, N = routed rows, S = shared experts):
+      router forward   T*d*s + E*d*s + 4*T*E + 8*T*k   (x and W_r read; logits, top-k indices and weights written)
+      permute          T*d*s + N*d*s + 8*T*k           (histogram, scatter and gather launches together)
+      combine          N*d*s + T*d*s + S*T*d*s + 8*T*k
+      combine backward T*d*s + 2*N*d*s + 8*T*k
+      unpermute        N*d*s + T*d*s + S*T*d*s + 4*T*k
+    The times are the warm-up steps' HIP events around every launch, which include the gap between
+    back-to-back launches (about 1-2 us here), so the rates are lower bounds of the kernels' own."""
+    s = 2 if cfg.dtype == "bf16" else 4
+    T, d, k, E, S, N = cfg.T, cfg.d, cfg.k, cfg.E, cfg.n_shared, n_routed
+    table = {
+        "route_fwd": (("route_fwd",), T * d * s + E * d * s + 4 * T * E + 8 * T * k),
+        "permute": (("permute_hist", "permute_scatter", "permute_gather"), T * d * s + N * d * s + 8 * T * k),
+        "combine": (("combine",), N * d * s + T * d * s + S * T * d * s + 8 * T * k),
+        "combine_bwd": (("combine_bwd",), T * d * s + 2 * N * d * s + 8 * T * k),
+        "unpermute": (("unpermute",), N * d * s + T * d * s + S * T * d * s + 4 * T * k),
+    }
+    out = {}
+    for step, (names, nbytes) in table.items():
+        if not all(n in kernels for n in names):
+            continue
+        us = sum(kernels[n]["avg_us"] for n in names)
+        gbs = nbytes / (us * 1e-6) / 1e9
+        out[step] = {"bytes": nbytes, "us": round(us, 2), "GB/s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    return out
+
+
 def memory_amortisation(P, parties=(1, 2, 4, 8)):
     """The per-party memory claim of Sec. 3 (experts sharded over n parties): one party's peak device memory for
     the expert layer's training step when it hosts all E experts or E/n of them. The row-space buffers keep their
@@ -299,6 +328,7 @@ def main():
         "roofline": roof,
         "kernels_warmup": {k: {"avg_us": round(v["avg_us"], 2), "per_step": v["launches_per_step"]}
                            for k, v in kernels.items()},
+        "hbm_steps_warmup": hbm_steps(cfg, n_routed, kernels),
     }
     out["expert_update"] = measure_expert_update(P, layer, w, args.steps)
     if not args.no_cpu_baseline:
