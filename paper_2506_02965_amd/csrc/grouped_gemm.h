@@ -164,14 +164,15 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs& p, int bid, TileIdx&
   return true;
 }
 
-// Tile plan of the row-ragged contractions (one workgroup of 512 threads: at most 511 groups): pre0 and pre1 =
-// m-tile prefixes for bm0- and bm1-row tiles; for bm1-row tiles also body1 = prefix of the m-tiles other than
-// the tails and tail1 = prefix of the tails (a last m-tile holding at most bm1 / 2 rows); order = groups by
-// decreasing row count (ties by index).
+// Tile plan of the row-ragged contractions (one workgroup of 512 threads: at most 511 groups): pre0, pre1 and
+// pre2 = m-tile prefixes for bm0-, bm1- and bm2-row tiles; for bm1-row tiles also body1 = prefix of the m-tiles
+// other than the tails and tail1 = prefix of the tails (a last m-tile holding at most bm1 / 2 rows); order =
+// groups by decreasing row count (ties by index).
 __global__ __launch_bounds__(512) void mtile_prefix_kernel(const int32_t* __restrict__ offsets, int Eloc, int S,
-                                                           int Tn, int bm0, int bm1, int32_t* __restrict__ pre0,
-                                                           int32_t* __restrict__ pre1, int32_t* __restrict__ body1,
-                                                           int32_t* __restrict__ tail1, int32_t* __restrict__ order);
+                                                           int Tn, int bm0, int bm1, int bm2,
+                                                           int32_t* __restrict__ pre0, int32_t* __restrict__ pre1,
+                                                           int32_t* __restrict__ body1, int32_t* __restrict__ tail1,
+                                                           int32_t* __restrict__ pre2, int32_t* __restrict__ order);
 
 // fp32 path (generic LDS-tiled MFMA 16x16x4 kernel)
 hipError_t ffn_fwd_f32(const moe_desc& d, const void* x, const void* xp, const int32_t* offsets, const void* wg,

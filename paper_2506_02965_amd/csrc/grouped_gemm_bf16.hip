@@ -489,13 +489,15 @@ static hipError_t run2(const GemmArgs& a, long tiles, hipStream_t s, const char*
 // Tile shapes (BM x BN, LDS stages, wavefronts) instantiated for every contraction. Two wavefronts
 // per SIMD are what keep the MFMA pipes busy: 4-wave 128x128 tiles run two workgroups per CU,
 // the larger tiles use 8 wavefronts in one workgroup.
+// 192-row tiles (K-contiguous A only: the row-ragged contractions) serve a contraction whose 256-row grid is
+// one partial round of the chip.
 enum TileShape { T128x128s2 = 0, T256x128w8, T128x256w8, T256x256w8, T256x256k32, T256x128k32, T128x128k32,
-                 T256x256w16, T256x256w16k32s4, T256x256w16k32s3, N_SHAPES };
-static const int kShapeBM[N_SHAPES] = {128, 256, 128, 256, 256, 256, 128, 256, 256, 256};
-static const int kShapeBN[N_SHAPES] = {128, 128, 256, 256, 256, 128, 128, 256, 256, 256};
+                 T256x256w16, T256x256w16k32s4, T256x256w16k32s3, T192x256w8, N_SHAPES };
+static const int kShapeBM[N_SHAPES] = {128, 256, 128, 256, 256, 256, 128, 256, 256, 256, 192};
+static const int kShapeBN[N_SHAPES] = {128, 128, 256, 256, 256, 128, 128, 256, 256, 256, 256};
 static const char* kShapeName[N_SHAPES] = {"128x128s2", "256x128w8", "128x256w8", "256x256w8", "256x256k32",
                                            "256x128k32", "128x128k32", "256x256w16", "256x256w16k32s4",
-                                           "256x256w16k32s3"};
+                                           "256x256w16k32s3", "192x256w8"};
 
 static const char* kKindName[6] = {"gemm_fwd_gate_up", "gemm_fwd_down", "gemm_bwd_dh", "gemm_bwd_dx",
                                    "gemm_wgrad_down", "gemm_wgrad_gate_up"};
@@ -533,12 +535,17 @@ static hipError_t run_shape(int shape, const GemmArgs& a, long tiles, hipStream_
     case T256x256w16: return run2<256, 256, 64, KIND, 2, 4, 4>(a, tiles, s, kKindName[KIND]);
     case T256x256w16k32s4: return run2<256, 256, 32, KIND, 4, 4, 4>(a, tiles, s, kKindName[KIND]);
     case T256x256w16k32s3: return run2<256, 256, 32, KIND, 3, 4, 4>(a, tiles, s, kKindName[KIND]);
+    case T192x256w8:
+      if constexpr (KindTraits<KIND>::a_kc) return run2<192, 256, 64, KIND, 2, 2, 4>(a, tiles, s, kKindName[KIND]);
+      return hipErrorInvalidValue;  // not selected for K-major A (fit_shape)
     default: return run2<256, 256, 64, KIND, 2, 2, 4>(a, tiles, s, kKindName[KIND]);
   }
 }
 
 // Default shape per contraction; PCMOE_GEMM_TILES="<kind>=<shape>,..." overrides (kind 0..5 as in
 // GemmKind, shape as in kShapeName), e.g. "0=256x256s2,5=128x256s3".
+static long mtile_bound2(const moe_desc& d, int bm);
+static int device_cus();
 static int tile_shape(int kind, const moe_desc& d) {
   static int table[6] = {-1, -1, -1, -1, -1, -1};
   static bool parsed = false;
@@ -558,7 +565,13 @@ static int tile_shape(int kind, const moe_desc& d) {
     }
   }
   if (table[kind] >= 0) return table[kind];
-  (void)d;
+  // FWD_DOWN (N = d_model): when its 256x256 grid is one partial round of the chip, 192-row tiles still fit one
+  // round and each costs about 3/4 of a 256-row tile. (The backward kinds run paired with a weight gradient,
+  // which shares their shape.)
+  if (kind == FWD_DOWN && d.d_model % 256 == 0) {
+    const long n = d.d_model / 256;
+    if (mtile_bound2(d, 256) * n <= device_cus() && mtile_bound2(d, 192) * n <= device_cus()) return T192x256w8;
+  }
   return T256x256w16;
 }
 
@@ -569,7 +582,7 @@ static long mtile_bound2(const moe_desc& d, int bm) {
 }
 
 static size_t plan_part(const moe_desc& d) { return align256((size_t)(d.local_count + d.n_shared + 1) * 4); }
-static size_t plan_bytes(const moe_desc& d) { return 5 * plan_part(d); }
+static size_t plan_bytes(const moe_desc& d) { return 6 * plan_part(d); }
 // saved = G|U [R, 2f], H [R, f], then the tile plan of the forward, which the backward reuses
 static size_t saved_plan_offset(const moe_desc& d) {
   const size_t R = (size_t)rows_total(d), es = elem_bytes(d);
@@ -588,10 +601,11 @@ struct Plan {
   int32_t* order;
   int32_t* body256;  // 256-row m-tiles other than the tails
   int32_t* tail256;  // 256-row tail m-tiles (at most 128 rows)
+  int32_t* pre192;
 };
 
-// The plan's arrays at `where`: m-tile prefixes for 128- and 256-row tiles, the heaviest-first group order, and
-// for 256-row tiles the prefixes without the tails and of the tails.
+// The plan's arrays at `where`: m-tile prefixes for 128-, 192- and 256-row tiles, the heaviest-first group order,
+// and for 256-row tiles the prefixes without the tails and of the tails.
 static Plan plan_at(const moe_desc& d, void* where) {
   Plan pl;
   pl.pre128 = (int32_t*)where;
@@ -599,13 +613,14 @@ static Plan plan_at(const moe_desc& d, void* where) {
   pl.order = (int32_t*)((char*)where + 2 * plan_part(d));
   pl.body256 = (int32_t*)((char*)where + 3 * plan_part(d));
   pl.tail256 = (int32_t*)((char*)where + 4 * plan_part(d));
+  pl.pre192 = (int32_t*)((char*)where + 5 * plan_part(d));
   return pl;
 }
 static Plan plan(const moe_desc& d, const int32_t* offsets, void* where, hipStream_t s) {
   Plan pl = plan_at(d, where);
   KernelTimer kt("ffn_plan", s);
   hipLaunchKernelGGL(mtile_prefix_kernel, dim3(1), dim3(512), 0, s, offsets, d.local_count, d.n_shared, d.T, 128, 256,
-                     pl.pre128, pl.pre256, pl.body256, pl.tail256, pl.order);
+                     192, pl.pre128, pl.pre256, pl.body256, pl.tail256, pl.pre192, pl.order);
   return pl;
 }
 
@@ -633,7 +648,7 @@ static int device_cus() {
 // A shape must tile M and N exactly (d_model, d_ff are multiples of 128): fall back to 128-wide sides.
 static int fit_shape(int sh, int M, int N) {
   int bm = kShapeBM[sh], bn = kShapeBN[sh];
-  if (M > 0 && M % bm) bm = 128;
+  if (M > 0 && (M % bm || bm == 192)) bm = 128;  // weight gradients (K-major A) take no 192-row tiles
   if (N % bn) bn = 128;
   if (bm == kShapeBM[sh] && bn == kShapeBN[sh]) return sh;
   const bool k32 = sh == T256x256k32 || sh == T256x128k32 || sh == T128x128k32;
@@ -661,7 +676,7 @@ static Prep prep_ragged(const moe_desc& d, GemmArgs a, const Plan& pl, int n_col
   // 256-row tiles in more than one round of the chip: tails after the others (see decode_tile); each XCD
   // rounds its share of both segments up, at most 16 workgroups more
   const bool split = bm == 256 && bound > device_cus();
-  a.mt_prefix = bm == 128 ? pl.pre128 : split ? pl.body256 : pl.pre256;
+  a.mt_prefix = bm == 128 ? pl.pre128 : bm == 192 ? pl.pre192 : split ? pl.body256 : pl.pre256;
   a.mt_tail = split ? pl.tail256 : nullptr;
   return Prep{sh, a, bound + (split ? 16 : 0)};
 }

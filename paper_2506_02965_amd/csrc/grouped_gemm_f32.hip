@@ -360,10 +360,11 @@ __global__ __launch_bounds__(64 * WM * WN) void grouped_gemm_kernel(GemmArgs p) 
 // m-tile prefixes over groups for two tile heights: pre[g] = sum_{g' < g} ceil(rows_g' / bm); and
 // the groups ordered by decreasing row count (ties by index).
 __global__ __launch_bounds__(512) void mtile_prefix_kernel(const int32_t* __restrict__ offsets, int Eloc, int S,
-                                                           int Tn, int bm0, int bm1, int32_t* __restrict__ pre0,
-                                                           int32_t* __restrict__ pre1, int32_t* __restrict__ body1,
-                                                           int32_t* __restrict__ tail1, int32_t* __restrict__ order) {
-  __shared__ int buf[4][2][512];
+                                                           int Tn, int bm0, int bm1, int bm2,
+                                                           int32_t* __restrict__ pre0, int32_t* __restrict__ pre1,
+                                                           int32_t* __restrict__ body1, int32_t* __restrict__ tail1,
+                                                           int32_t* __restrict__ pre2, int32_t* __restrict__ order) {
+  __shared__ int buf[5][2][512];
   __shared__ int rows_s[512];
   const int g = threadIdx.x;
   const int G = Eloc + S;
@@ -376,6 +377,7 @@ __global__ __launch_bounds__(512) void mtile_prefix_kernel(const int32_t* __rest
   buf[1][0][g] = (rows + bm1 - 1) / bm1;
   buf[2][0][g] = (rows + bm1 - 1) / bm1 - is_tail;
   buf[3][0][g] = is_tail;
+  buf[4][0][g] = (rows + bm2 - 1) / bm2;
   rows_s[g] = rows;
   __syncthreads();
   if (g < G) {
@@ -386,7 +388,7 @@ __global__ __launch_bounds__(512) void mtile_prefix_kernel(const int32_t* __rest
   int cur = 0;
   for (int off = 1; off < 512; off <<= 1) {
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
+    for (int w = 0; w < 5; ++w) {
       int x = buf[w][cur][g];
       if (g >= off) x += buf[w][cur][g - off];
       buf[w][cur ^ 1][g] = x;
@@ -399,6 +401,7 @@ __global__ __launch_bounds__(512) void mtile_prefix_kernel(const int32_t* __rest
     pre1[g] = (g == 0) ? 0 : buf[1][cur][g - 1];
     body1[g] = (g == 0) ? 0 : buf[2][cur][g - 1];
     tail1[g] = (g == 0) ? 0 : buf[3][cur][g - 1];
+    pre2[g] = (g == 0) ? 0 : buf[4][cur][g - 1];
   }
 }
 
