@@ -92,18 +92,20 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs& p, int bid, TileIdx&
   int L;
   bool tail = false;
   if (RAGGED) {
-    const int per_xcd = (total + 7) >> 3;
-    const int lb = bid >> 3;
-    if (lb < per_xcd) {
-      L = (bid & 7) * per_xcd + lb;
+    // XCD x = bid % 8 takes the run [x * q + min(x, r), ...) of q or q + 1 tiles (total = 8 q + r) of each
+    // segment: the counts differ by at most one between XCDs
+    const int x = bid & 7, lb = bid >> 3;
+    const int q = total >> 3, r = total & 7;
+    const int cnt = q + (x < r ? 1 : 0);
+    if (lb < cnt) {
+      L = x * q + min(x, r) + lb;
     } else {
       if (!split) return false;
       const int ptot = wave_pick(tl, G) * p.n_tiles;
-      const int per_xcd_t = (ptot + 7) >> 3;
-      const int lt = lb - per_xcd;
-      if (lt >= per_xcd_t) return false;
-      L = (bid & 7) * per_xcd_t + lt;
-      if (L >= ptot) return false;
+      const int qt = ptot >> 3, rt = ptot & 7;
+      const int lt = lb - cnt;
+      if (lt >= qt + (x < rt ? 1 : 0)) return false;
+      L = x * qt + min(x, rt) + lt;
       tail = true;
     }
   } else {

@@ -666,16 +666,18 @@ struct Prep {
   long tiles;
 };
 
-// Ragged-M contraction with n_cols output columns in the tile grid (FWD_GU: gate and up columns).
+// Ragged-M contraction with n_cols output columns in the tile grid (FWD_GU: gate and up columns). tails_last:
+// split off the tails even when the grid is one round (a paired launch, where it shares the chip).
 template <int KIND>
-static Prep prep_ragged(const moe_desc& d, GemmArgs a, const Plan& pl, int n_cols) {
+static Prep prep_ragged(const moe_desc& d, GemmArgs a, const Plan& pl, int n_cols, bool tails_last = false) {
   const int sh = fit_shape(tile_shape(KIND, d), 0, n_cols);
   const int bm = kShapeBM[sh], bn = kShapeBN[sh];
   a.n_tiles = n_cols / bn;  // FWD_GU: n_cols = 2f, each tile holds bn/2 gate and bn/2 up columns
   const long bound = mtile_bound2(d, bm) * a.n_tiles;
-  // 256-row tiles in more than one round of the chip: tails after the others (see decode_tile); each XCD
-  // rounds its share of both segments up, at most 16 workgroups more
-  const bool split = bm == 256 && bound > device_cus();
+  // 256-row tiles in more than one round of the chip, or sharing it with another contraction: tails after the
+  // others (see decode_tile), so that every XCD gets an even share of both; its share of each segment is rounded
+  // up, at most 16 workgroups more
+  const bool split = bm == 256 && (tails_last || bound > device_cus());
   a.mt_prefix = bm == 128 ? pl.pre128 : bm == 192 ? pl.pre192 : split ? pl.body256 : pl.pre256;
   a.mt_tail = split ? pl.tail256 : nullptr;
   return Prep{sh, a, bound + (split ? 16 : 0)};
@@ -760,7 +762,7 @@ hipError_t launch_ffn_bwd(const moe_desc& d, const void* x, const void* xp, cons
                                            prep_wgrad<WG_DOWN>(d, a_wd, pl, d.d_model, d.d_ff), s,
                                            "gemm_bwd_dh+wgrad_down");
   if (e != hipSuccess) return e;
-  return run_pair<BWD_DX, WG_GU>(prep_ragged<BWD_DX>(d, a_dx, pl, d.d_model),
+  return run_pair<BWD_DX, WG_GU>(prep_ragged<BWD_DX>(d, a_dx, pl, d.d_model, pair_enabled()),
                                  prep_wgrad<WG_GU>(d, a_wgu, pl, 2 * d.d_ff, d.d_model), s,
                                  "gemm_bwd_dx+wgrad_gate_up");
 }
