@@ -45,6 +45,16 @@ def small_cases():
     C["forced_empty_experts"] = (LayerConfig("fe", T=512, d=256, f=256, E=8, k=2, bias="forced_empty", seed=19),
                                  forced_empty)
 
+    # a party whose hosted experts (4..7) receive no token: every routed group of its grouped GEMMs is empty
+    # (N_loc = 0), alone and beside a shared expert
+    def no_hosted_tokens(inp):
+        inp.logit_bias[0, 4:8] = -1e4
+    C["shard_without_tokens"] = (LayerConfig("nt", T=512, d=256, f=256, E=8, k=2, local_begin=4, local_count=4,
+                                             router_backward=False, bias="forced_empty", seed=27), no_hosted_tokens)
+    C["shard_without_tokens_shared"] = (LayerConfig("nts", T=512, d=256, f=256, E=8, k=2, local_begin=4,
+                                                    local_count=4, n_shared=1, router_backward=False,
+                                                    bias="forced_empty", seed=28), no_hosted_tokens)
+
     def all_to_one(inp):
         inp.logit_bias[0, 2] = 1e4
     C["all_tokens_one_expert"] = (LayerConfig("a1", T=384, d=128, f=256, E=4, k=1, bias="forced_empty", seed=20),
