@@ -26,6 +26,7 @@ struct GemmArgs {
   void* dgu;                  // [R, 2f] dG|dU
   void* out;                  // y_perm / dx_perm / dW_down / dW_gate
   void* out2;                 // dW_up (WG_GU)
+  int wg_interleave;          // weight gradients: tile L belongs to group order[L % G] (round-robin over groups)
 };
 
 template <int KIND> struct KindTraits;
@@ -87,8 +88,8 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs& p, int bid, TileIdx&
   // weights of few groups). With mt_tail, a group's last m-tile holding at most half a tile of rows (its
   // empty wavefronts skip their MFMAs) is left out of that run: each XCD takes its share of those cheap
   // tiles after its share of the others, so that they fill the last, partial round of tiles. Weight-gradient
-  // tiles cost K = rows of their group, heaviest groups first; they are dealt round-robin over the XCDs so
-  // that the long ones spread out.
+  // tiles cost K = rows of their group, heaviest groups first (or, with wg_interleave, one tile of each group in
+  // turn); they are dealt round-robin over the XCDs so that the long ones spread out.
   int L;
   bool tail = false;
   if (RAGGED) {
@@ -150,9 +151,15 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs& p, int bid, TileIdx&
     l = L - p0 * p.n_tiles;
     n_mt = wave_pick(pre, g + 1) - p0;
   } else {
-    const int rank = L / (p.m_tiles * p.n_tiles);  // heaviest groups first: their long K loops start early
+    int rank;
+    if (p.wg_interleave) {  // one tile of every group in turn, heaviest first within a turn
+      rank = L % G;
+      l = L / G;
+    } else {                // heaviest groups first: their long K loops start early
+      rank = L / (p.m_tiles * p.n_tiles);
+      l = L - rank * p.m_tiles * p.n_tiles;
+    }
     t.g = p.order ? wave_pick(ord, rank) : rank;
-    l = L - rank * p.m_tiles * p.n_tiles;
     n_mt = p.m_tiles;
   }
   const bool routed = t.g < p.Eloc;

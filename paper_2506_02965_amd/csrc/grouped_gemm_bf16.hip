@@ -687,6 +687,13 @@ template <int KIND>
 static Prep prep_wgrad(const moe_desc& d, GemmArgs a, const Plan& pl, int M, int N) {
   const int sh = fit_shape(tile_shape(KIND, d), M, N);
   a.order = pl.order;
+  // dW_gate|dW_up takes its groups round-robin: it shares its launch with dX, whose tiles read the same dG|dU
+  // rows, and every group's rows then get pulled into the caches early, not only the heaviest groups'.
+  // PCMOE_WGRR=<bit mask of kinds> overrides.
+  {
+    const char* e = getenv("PCMOE_WGRR");
+    a.wg_interleave = e ? (atoi(e) >> KIND) & 1 : (KIND == WG_GU ? 1 : 0);
+  }
   a.m_tiles = M / kShapeBM[sh];
   a.n_tiles = N / kShapeBN[sh];
   return Prep{sh, a, (long)(d.local_count + d.n_shared) * a.m_tiles * a.n_tiles};
