@@ -26,7 +26,8 @@ struct GemmArgs {
   void* dgu;                  // [R, 2f] dG|dU
   void* out;                  // y_perm / dx_perm / dW_down / dW_gate
   void* out2;                 // dW_up (WG_GU)
-  int wg_interleave;          // weight gradients: tile L belongs to group order[L % G] (round-robin over groups)
+  int wg_interleave;          // weight gradients: with near-equal groups (order[G] = 1), tile L belongs to group
+                              // order[L % G] (round-robin over groups)
 };
 
 template <int KIND> struct KindTraits;
@@ -77,7 +78,7 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs& p, int bid, TileIdx&
     if (s < ns) {
       if (RAGGED && i <= G) pre[s] = p.mt_prefix[i];
       if (split && i <= G) tl[s] = p.mt_tail[i];
-      if (!RAGGED && p.order && i < G) ord[s] = p.order[i];
+      if (!RAGGED && p.order && i <= G) ord[s] = p.order[i];
       if (i <= p.Eloc) off[s] = p.offsets[i];
     }
   }
@@ -152,7 +153,7 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs& p, int bid, TileIdx&
     n_mt = wave_pick(pre, g + 1) - p0;
   } else {
     int rank;
-    if (p.wg_interleave) {  // one tile of every group in turn, heaviest first within a turn
+    if (p.wg_interleave && p.order && wave_pick(ord, G) != 0) {  // one tile of each group in turn, heaviest first
       rank = L % G;
       l = L / G;
     } else {                // heaviest groups first: their long K loops start early
@@ -176,7 +177,8 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs& p, int bid, TileIdx&
 // Tile plan of the row-ragged contractions (one workgroup of 512 threads: at most 511 groups): pre0, pre1 and
 // pre2 = m-tile prefixes for bm0-, bm1- and bm2-row tiles; for bm1-row tiles also body1 = prefix of the m-tiles
 // other than the tails and tail1 = prefix of the tails (a last m-tile holding at most bm1 / 2 rows); order =
-// groups by decreasing row count (ties by index).
+// groups by decreasing row count (ties by index), and order[G] = 1 when all groups' row counts lie within 25% of
+// the largest (0 otherwise).
 __global__ __launch_bounds__(512) void mtile_prefix_kernel(const int32_t* __restrict__ offsets, int Eloc, int S,
                                                            int Tn, int bm0, int bm1, int bm2,
                                                            int32_t* __restrict__ pre0, int32_t* __restrict__ pre1,

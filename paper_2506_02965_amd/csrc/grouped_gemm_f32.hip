@@ -385,6 +385,14 @@ __global__ __launch_bounds__(512) void mtile_prefix_kernel(const int32_t* __rest
     for (int h = 0; h < G; ++h) rank += (rows_s[h] > rows) || (rows_s[h] == rows && h < g);
     order[rank] = g;
   }
+  if (g == 0) {  // order[G] = 1 when every group's row count is within 25% of the largest
+    int lo = rows_s[0], hi = rows_s[0];
+    for (int h = 1; h < G; ++h) {
+      lo = min(lo, rows_s[h]);
+      hi = max(hi, rows_s[h]);
+    }
+    order[G] = (G > 0 && 4 * hi <= 5 * lo) ? 1 : 0;
+  }
   int cur = 0;
   for (int off = 1; off < 512; off <<= 1) {
 #pragma unroll
