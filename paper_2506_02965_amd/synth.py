@@ -7,13 +7,13 @@ precision and describes the five workload shapes.
 Workloads (shapes stand in for the paper's fine-tuning runs, whose model, data and layer sizes
 are not published; Sec. 4 setup, Table 1):
 
-  cfg1  fp32 forward only,  T=512,  d=256,  f=512,   E=8,  top-2
-  cfg2  bf16 fwd+bwd,       T=4096, d=1024, f=2816,  E=16, top-2
-  cfg3  bf16 fwd+bwd shard, T=8192 (4 parties x 2048), d=2048, f=1408, E=64 global,
-        this GPU hosts experts 0..15, top-4, per-party N(0,1) logit bias
-  cfg4  bf16 fwd+bwd,       T=8192, d=4096, f=14336, E=8,  top-2
-  cfg5  bf16 fwd+bwd,       T=16384, d=2048, f=1408, E=64 routed top-6 + 2 shared experts,
-        logit bias log p_e with p ~ Zipf(s=1.1) over experts
+  1  fp32 forward only,  T=512,  d=256,  f=512,   E=8,  top-2
+  2  bf16 fwd+bwd,       T=4096, d=1024, f=2816,  E=16, top-2 (the benchmark's workload)
+  3  bf16 fwd+bwd shard, T=8192 (4 parties x 2048), d=2048, f=1408, E=64 global,
+     this GPU hosts experts 0..15, top-4, per-party N(0,1) logit bias
+  4  bf16 fwd+bwd,       T=8192, d=4096, f=14336, E=8,  top-2
+  5  bf16 fwd+bwd,       T=16384, d=2048, f=1408, E=64 routed top-6 + 2 shared experts,
+     logit bias log p_e with p ~ Zipf(s=1.1) over experts
 
 Draw recipe: every tensor has its own numpy PCG64 stream keyed by (seed, tag, expert), drawn
 as float32 standard normals, scaled in float32, and for bf16 workloads rounded once to
@@ -71,13 +71,13 @@ class LayerConfig:
 
 
 CONFIGS = {
-    1: LayerConfig("cfg1_fp32_fwd_T512_d256_f512_E8_k2", T=512, d=256, f=512, E=8, k=2,
+    1: LayerConfig("fp32_fwd_T512_d256_f512_E8_k2", T=512, d=256, f=512, E=8, k=2,
                    dtype="f32", backward=False, seed=0),
-    2: LayerConfig("cfg2_bf16_T4096_d1024_f2816_E16_k2", T=4096, d=1024, f=2816, E=16, k=2, seed=1),
-    3: LayerConfig("cfg3_bf16_shard_T8192_d2048_f1408_E64loc16_k4", T=8192, d=2048, f=1408, E=64, k=4,
+    2: LayerConfig("bf16_T4096_d1024_f2816_E16_k2", T=4096, d=1024, f=2816, E=16, k=2, seed=1),
+    3: LayerConfig("bf16_shard_T8192_d2048_f1408_E64loc16_k4", T=8192, d=2048, f=1408, E=64, k=4,
                    local_begin=0, local_count=16, router_backward=False, bias="party", parties=4, seed=2),
-    4: LayerConfig("cfg4_bf16_T8192_d4096_f14336_E8_k2", T=8192, d=4096, f=14336, E=8, k=2, seed=3),
-    5: LayerConfig("cfg5_bf16_T16384_d2048_f1408_E64_k6_S2", T=16384, d=2048, f=1408, E=64, k=6,
+    4: LayerConfig("bf16_T8192_d4096_f14336_E8_k2", T=8192, d=4096, f=14336, E=8, k=2, seed=3),
+    5: LayerConfig("bf16_T16384_d2048_f1408_E64_k6_S2", T=16384, d=2048, f=1408, E=64, k=6,
                    n_shared=2, bias="zipf", seed=4),
 }
 
@@ -105,7 +105,7 @@ def _store(a: np.ndarray, dtype: str) -> np.ndarray:
 
 
 def zipf_logit_bias(E: int, s: float = 1.1) -> np.ndarray:
-    """Per-expert additive logit bias log p_e with p_e proportional to (e+1)^-s (input recipe, cfg5)."""
+    """Per-expert additive logit bias log p_e with p_e proportional to (e+1)^-s (input recipe of the Zipf-skewed E=64 workload)."""
     r = np.arange(1, E + 1, dtype=np.float64)
     p = r ** (-s)
     p /= p.sum()

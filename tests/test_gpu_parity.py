@@ -1,9 +1,9 @@
 """Parity of the HIP layer (through the C ABI) with the CPU oracle on the GPU.
 
 Small cases run the whole oracle and compare every output element by element; they span several
-GEMM tiles and ragged tails. The five workload configurations run at full size in the launch
-configuration the benchmark times; configs 4 and 5 are checked on sampled outputs plus
-properties. Routing indices and the permutation are bit-exact everywhere."""
+GEMM tiles and ragged tails. The five workloads run at full size in the launch configuration the
+benchmark times; the two largest (T=8192 d=4096 f=14336, and T=16384 with 64 experts) are checked on
+sampled outputs plus properties. Routing indices and the permutation are bit-exact everywhere."""
 import dataclasses
 
 import numpy as np
@@ -18,17 +18,17 @@ pytestmark = pytest.mark.gpu
 
 def small_cases():
     C = {}
-    C["cfg1_f32_full"] = (CONFIGS[1], None)
+    C["fp32_T512_full"] = (CONFIGS[1], None)
     C["f32_fwd_bwd_shared"] = (LayerConfig("f32b", T=300, d=256, f=384, E=8, k=2, n_shared=1, dtype="f32",
                                            seed=10), None)
-    C["cfg2_like_T1000"] = (LayerConfig("c2s", T=1000, d=256, f=384, E=16, k=2, seed=11), None)
-    C["cfg3_like_shard"] = (LayerConfig("c3s", T=1024, d=256, f=256, E=64, k=4, local_begin=0, local_count=16,
+    C["bf16_T1000_E16"] = (LayerConfig("c2s", T=1000, d=256, f=384, E=16, k=2, seed=11), None)
+    C["shard_E64_loc16"] = (LayerConfig("c3s", T=1024, d=256, f=256, E=64, k=4, local_begin=0, local_count=16,
                                         router_backward=False, bias="party", parties=4, seed=12), None)
-    C["cfg3_like_shard_mid"] = (LayerConfig("c3m", T=1024, d=256, f=256, E=64, k=4, local_begin=16,
+    C["shard_E64_loc16_mid"] = (LayerConfig("c3m", T=1024, d=256, f=256, E=64, k=4, local_begin=16,
                                             local_count=16, router_backward=False, bias="party", parties=4,
                                             seed=12), None)
-    C["cfg4_like"] = (LayerConfig("c4s", T=512, d=512, f=1024, E=8, k=2, seed=13), None)
-    C["cfg5_like_shared_zipf"] = (LayerConfig("c5s", T=1024, d=256, f=384, E=64, k=6, n_shared=2, bias="zipf",
+    C["bf16_d512_f1024_E8"] = (LayerConfig("c4s", T=512, d=512, f=1024, E=8, k=2, seed=13), None)
+    C["E64_k6_shared_zipf"] = (LayerConfig("c5s", T=1024, d=256, f=384, E=64, k=6, n_shared=2, bias="zipf",
                                               seed=14), None)
     C["renormalize0"] = (LayerConfig("r0", T=512, d=256, f=256, E=16, k=4, renormalize=False, seed=15), None)
     C["k1"] = (LayerConfig("k1", T=256, d=128, f=128, E=4, k=1, seed=16), None)
@@ -113,21 +113,21 @@ def test_deterministic_bits():
         assert torch.equal(getattr(a, n), getattr(b, n)), n
 
 
-@pytest.mark.parametrize("c", [1, 2, 3])
-def test_config_full_size(c):
+@pytest.mark.parametrize("c", [1, 2, 3], ids=lambda c: CONFIGS[c].name)
+def test_workload_full_size(c):
     cfg = CONFIGS[c]
-    log(f"[parity] full-size config {c}: {cfg.name}")
+    log(f"[parity] full-size workload {cfg.name}")
     inp = make_inputs(cfg, with_dy=True)
     layer, _ = run_gpu(cfg, inp)
     errs = check_full(cfg, inp, layer)
-    log(f"[parity] config {c}: " + " ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+    log(f"[parity] {cfg.name}: " + " ".join(f"{k}={v:.2e}" for k, v in errs.items()))
 
 
-@pytest.mark.parametrize("c", [4, 5])
-def test_config_full_size_sampled(c):
+@pytest.mark.parametrize("c", [4, 5], ids=lambda c: CONFIGS[c].name)
+def test_workload_full_size_sampled(c):
     cfg = CONFIGS[c]
-    log(f"[parity] full-size config {c} (sampled): {cfg.name}")
+    log(f"[parity] full-size workload {cfg.name} (sampled)")
     inp = make_inputs(cfg, with_dy=True)
     layer, _ = run_gpu(cfg, inp)
     errs = check_sampled(cfg, inp, layer)
-    log(f"[parity] config {c}: " + " ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+    log(f"[parity] {cfg.name}: " + " ".join(f"{k}={v:.2e}" for k, v in errs.items()))

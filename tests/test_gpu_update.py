@@ -113,7 +113,7 @@ def test_update_zero_gradient_fixed_point():
     assert not Mo.any() and not Ve.any()
 
 
-def test_update_config2_sampled():
+def test_update_E16_f2816_d1024_sampled():
     """16 experts, f=2816, d=1024 (the benchmark's shapes), bf16 with master, AdamW: a sample of
     200k parameters against the oracle."""
     G, f, d = 16, 2816, 1024
@@ -130,7 +130,7 @@ def test_update_config2_sampled():
     g_flat = torch.cat([x.reshape(-1) for x in Gd]).float()
     src, m0, v0, g0 = (t[idx].double().cpu().numpy() for t in (master, Mo, Ve, g_flat))
     desc = P.make_desc(T=4096, d_model=d, d_ff=f, n_experts=G, top_k=2, dtype="bf16")
-    log("update config2 sampled")
+    log("update E=16 f=2816 d=1024 sampled")
     P.moe_expert_update(desc, P.make_opt(kind="adamw", lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1,
                                          step=4), *W, *Gd, master, Mo, Ve)
     torch.cuda.synchronize()
