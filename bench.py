@@ -1,6 +1,6 @@
 """Benchmark of the MoE expert layer (forward + backward) on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2] [--no-cpu-baseline]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 
 One step is one pass of the whole layer over one batch of resident synthetic inputs:
 route -> permute -> expert FFN forward -> combine -> combine backward -> expert FFN backward
@@ -180,7 +180,7 @@ def memory_amortisation(P, parties=(1, 2, 4, 8)):
     import dataclasses
     import torch
     from paper_2506_02965_amd.layer import MoELayer, upload, training_footprint
-    from paper_2506_02965_amd.synth import CONFIGS, make_inputs
+    from paper_2506_02965_amd.synth import make_inputs
     base = dataclasses.replace(CONFIGS[3], bias=None, router_backward=True, local_begin=0)
     rows = []
     for n in parties:
@@ -217,14 +217,25 @@ def memory_amortisation(P, parties=(1, 2, 4, 8)):
             "data": "synthetic", "rows": rows}
 
 
+def pick_workload(key: str):
+    from paper_2506_02965_amd.synth import CONFIGS
+    for i, c in CONFIGS.items():
+        if key in (c.name, str(i)):
+            return c
+    raise SystemExit(f"unknown workload {key!r}; known: " + ", ".join(c.name for c in CONFIGS.values()))
+
+
 def main():
+    from paper_2506_02965_amd.synth import CONFIGS
+    WORKLOADS = list(CONFIGS.values())
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     # The first ~60 steps (~50 ms) of a fresh process run up to 7% slower than the steady state that follows;
     # the default warm-up covers them.
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=100)
-    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--workload", "--config", dest="workload", default="bf16_T4096_d1024_f2816_E16_k2",
+                    help="workload name (" + ", ".join(c.name for c in WORKLOADS) + ") or its position 1-5 in that list")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--memory", action="store_true",
                     help="instead of the benchmark: peak device memory of one party's expert-layer training step "
@@ -242,7 +253,7 @@ def main():
     import torch
     from paper_2506_02965_amd import pcmoe as P
     from paper_2506_02965_amd.layer import MoELayer, upload
-    from paper_2506_02965_amd.synth import CONFIGS, make_inputs
+    from paper_2506_02965_amd.synth import make_inputs
 
     P.lib()
     if args.memory:
@@ -255,7 +266,7 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    cfg = CONFIGS[args.config]
+    cfg = pick_workload(args.workload)
     inp = make_inputs(cfg, with_dy=True)
     w = upload(inp, device="cuda")
     layer = MoELayer(cfg, backward=True)
