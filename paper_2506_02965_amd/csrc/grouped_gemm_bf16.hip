@@ -473,12 +473,8 @@ static hipError_t run2(const GemmArgs& a, long tiles, hipStream_t s, const char*
   using C = Cfg2<BM, BN, BK, STAGES, WM, WN>;
   static_assert(C::LDS <= 160 * 1024, "LDS budget of one CU");
   auto kern = gemm_bf16_kernel<BM, BN, BK, KIND, STAGES, WM, WN>;
-  static bool attr = false;
-  if (!attr) {
-    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
-    if (e != hipSuccess) return e;
-    attr = true;
-  }
+  static std::atomic<uint64_t> lds_set{0};
+  if (hipError_t e = lds_limit_once((const void*)kern, C::LDS, lds_set); e != hipSuccess) return e;
   const int grid = (int)((tiles + 7) / 8 * 8);
   if (grid <= 0) return hipSuccess;
   KernelTimer kt(name, s);
@@ -508,12 +504,8 @@ static hipError_t run_pair2(const GemmArgs& a, long tiles_a, const GemmArgs& b, 
   using C = Cfg2<BM, BN, BK, STAGES, WM, WN>;
   static_assert(C::LDS <= 160 * 1024, "LDS budget of one CU");
   auto kern = gemm_bf16_pair_kernel<BM, BN, BK, KA, KB, STAGES, WM, WN>;
-  static bool attr = false;
-  if (!attr) {
-    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
-    if (e != hipSuccess) return e;
-    attr = true;
-  }
+  static std::atomic<uint64_t> lds_set{0};
+  if (hipError_t e = lds_limit_once((const void*)kern, C::LDS, lds_set); e != hipSuccess) return e;
   // grid_a a multiple of 8 keeps each workgroup of the second contraction on the XCD its index implies
   const int grid_a = (int)((tiles_a + 7) / 8 * 8);
   const int grid = grid_a + (int)tiles_b;
@@ -547,13 +539,11 @@ static hipError_t run_shape(int shape, const GemmArgs& a, long tiles, hipStream_
 static long mtile_bound2(const moe_desc& d, int bm);
 static int device_cus();
 static int tile_shape(int kind, const moe_desc& d) {
-  static int table[6] = {-1, -1, -1, -1, -1, -1};
-  static bool parsed = false;
-  if (!parsed) {
-    parsed = true;
-    if (const char* env = getenv("PCMOE_GEMM_TILES")) {
-      const char* p = env;
-      while (*p) {
+  struct Overrides {  // parsed once (thread-safe static initialisation)
+    int table[6] = {-1, -1, -1, -1, -1, -1};
+    Overrides() {
+      const char* p = getenv("PCMOE_GEMM_TILES");
+      while (p && *p) {
         int k = *p - '0';
         if (k >= 0 && k < 6 && p[1] == '=') {
           for (int sh = 0; sh < N_SHAPES; ++sh)
@@ -563,8 +553,9 @@ static int tile_shape(int kind, const moe_desc& d) {
         if (*p == ',') ++p;
       }
     }
-  }
-  if (table[kind] >= 0) return table[kind];
+  };
+  static const Overrides ov;
+  if (ov.table[kind] >= 0) return ov.table[kind];
   // FWD_DOWN (N = d_model): when its 256x256 grid is one partial round of the chip, 192-row tiles still fit one
   // round and each costs about 3/4 of a 256-row tile. (The backward kinds run paired with a weight gradient,
   // which shares their shape.)
@@ -634,14 +625,16 @@ static GemmArgs args_for(const moe_desc& d, const int32_t* offsets) {
 
 // Compute units of the current device (queried once per device).
 static int device_cus() {
-  static int cus[64] = {0};
+  static std::atomic<int> cus[64];  // 0 = not queried yet
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cus[dev] <= 0) {
+  int c = cus[dev].load(std::memory_order_relaxed);
+  if (c <= 0) {
     int n = 0;
-    cus[dev] = (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0) ? n : 256;
+    c = (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0) ? n : 256;
+    cus[dev].store(c, std::memory_order_relaxed);
   }
-  return cus[dev];
+  return c;
 }
 
 // Ragged-M contraction: n_cols output columns of the tile grid (FWD_GU: gate columns, two per pair).
@@ -690,10 +683,11 @@ static Prep prep_wgrad(const moe_desc& d, GemmArgs a, const Plan& pl, int M, int
   // dW_gate|dW_up takes its groups round-robin: it shares its launch with dX, whose tiles read the same dG|dU
   // rows, and every group's rows then get pulled into the caches early, not only the heaviest groups'.
   // PCMOE_WGRR=<bit mask of kinds> overrides.
-  {
+  static const int wgrr = [] {
     const char* e = getenv("PCMOE_WGRR");
-    a.wg_interleave = e ? (atoi(e) >> KIND) & 1 : (KIND == WG_GU ? 1 : 0);
-  }
+    return e ? atoi(e) : -1;
+  }();
+  a.wg_interleave = wgrr >= 0 ? (wgrr >> KIND) & 1 : (KIND == WG_GU ? 1 : 0);
   a.m_tiles = M / kShapeBM[sh];
   a.n_tiles = N / kShapeBN[sh];
   return Prep{sh, a, (long)(d.local_count + d.n_shared) * a.m_tiles * a.n_tiles};
@@ -705,11 +699,10 @@ static hipError_t run(const Prep& p, hipStream_t s) {
 
 // PCMOE_PAIR=0 launches the paired contractions one after the other instead.
 static bool pair_enabled() {
-  static int on = -1;
-  if (on < 0) {
+  static const bool on = [] {
     const char* env = getenv("PCMOE_PAIR");
-    on = !(env && env[0] == '0');
-  }
+    return !(env && env[0] == '0');
+  }();
   return on;
 }
 

@@ -421,12 +421,8 @@ template <typename T, int KIND>
 static hipError_t run_gemm(const GemmArgs& a, int grid, hipStream_t s, const char* name) {
   using Cf = TileCfg<T, T_BM, T_BN, T_WM, T_WN>;
   auto kern = grouped_gemm_kernel<T, T_BM, T_BN, T_WM, T_WN, KIND>;
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, Cf::LDS);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
+  static std::atomic<uint64_t> lds_set{0};
+  if (hipError_t e = lds_limit_once((const void*)kern, Cf::LDS, lds_set); e != hipSuccess) return e;
   if (grid <= 0) return hipSuccess;
   KernelTimer kt(name, s);
   hipLaunchKernelGGL(kern, dim3(grid), dim3(Cf::NT), Cf::LDS, s, a);

@@ -1,5 +1,6 @@
 // Private helpers of the pcmoe HIP library (gfx950 / CDNA4). Not part of the ABI.
 #pragma once
+#include <atomic>
 #include <type_traits>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -114,6 +115,19 @@ struct KernelTimer {
   hipStream_t stream;
   void* slot;
 };
+
+// Raises a kernel's dynamic-LDS limit to `bytes` the first time it is launched on a device. `done` (one per
+// kernel) holds a bit per device index below 64; concurrent first calls both set the same value, which is
+// harmless. Returns hipSuccess or the runtime's error (then retried on the next call).
+inline hipError_t lds_limit_once(const void* kern, int bytes, std::atomic<uint64_t>& done) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) dev = 0;
+  const uint64_t bit = (dev >= 0 && dev < 64) ? (uint64_t)1 << dev : 0;
+  if (bit && (done.load(std::memory_order_acquire) & bit)) return hipSuccess;
+  const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e == hipSuccess) done.fetch_or(bit, std::memory_order_release);
+  return e;
+}
 
 // Launchers (defined next to their kernels). All return hipSuccess or the launch error.
 hipError_t launch_route_fwd(const moe_desc& d, const void* x, const void* wr, const float* bias, int bias_groups,

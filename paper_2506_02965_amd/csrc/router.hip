@@ -211,8 +211,8 @@ static hipError_t route_fwd_t(const moe_desc& d, const void* x, const void* wr, 
   do {                                                                                                          \
     const size_t lds = (size_t)W * 16 * (16 * NET + 1) * sizeof(double);                                       \
     if (lds > 65536) {                                                                                          \
-      hipError_t e_ = hipFuncSetAttribute((const void*)route_fwd_kernel<T, NET, W>,                              \
-                                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);                \
+      static std::atomic<uint64_t> lds_set_{0};                                                                 \
+      hipError_t e_ = lds_limit_once((const void*)route_fwd_kernel<T, NET, W>, (int)lds, lds_set_);             \
       if (e_ != hipSuccess) return e_;                                                                          \
     }                                                                                                           \
     hipLaunchKernelGGL((route_fwd_kernel<T, NET, W>), grid, dim3(64 * W), lds, s, (const T*)x, (const T*)wr,     \
