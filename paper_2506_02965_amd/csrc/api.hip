@@ -2,6 +2,7 @@
 // error reporting and the optional per-kernel event timing. Kernels live in the other files.
 #include "pcmoe_internal.h"
 
+#include <atomic>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -82,7 +83,7 @@ moe_status check_desc(const moe_desc* d) {
 // ------------------------------------------------------------------ per-kernel timing
 struct TimingState {
   std::mutex mu;
-  bool on = false;
+  std::atomic<bool> on{false};  // read without the lock on every launch (the common case: timing off)
   std::string only;  // record only launches with this name (empty: all)
   struct Rec {
     std::string name;
@@ -101,8 +102,9 @@ TimingState& timing() {
 namespace pcmoe {
 KernelTimer::KernelTimer(const char* n, hipStream_t s) : name(n), stream(s), slot(nullptr) {
   TimingState& ts = timing();
+  if (!ts.on.load(std::memory_order_acquire)) return;
   std::lock_guard<std::mutex> lk(ts.mu);
-  if (!ts.on) return;
+  if (!ts.on.load(std::memory_order_relaxed)) return;
   if (!ts.only.empty() && ts.only != n) return;
   hipEvent_t a = nullptr, b = nullptr;
   if (ts.pool.size() >= 2) {
@@ -282,7 +284,7 @@ moe_status moe_kernel_timing(int enable) {
     ts.pool.push_back(r.b);
   }
   ts.recs.clear();
-  ts.on = enable != 0;
+  ts.on.store(enable != 0, std::memory_order_release);
   return MOE_OK;
 }
 

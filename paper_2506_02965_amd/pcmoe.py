@@ -92,10 +92,16 @@ def last_error() -> str:
 
 
 def _ptr(t) -> Optional[int]:
+    """Device address of a tensor (or a raw integer address, passed through). A host tensor or a strided view
+    would be read as if it were a dense device buffer, so both are refused here."""
     if t is None:
         return None
     if isinstance(t, int):
         return t
+    if not t.is_cuda:
+        raise ValueError(f"expected a GPU tensor, got one on {t.device}")
+    if not t.is_contiguous():
+        raise ValueError(f"expected a contiguous tensor, got shape {tuple(t.shape)} strides {t.stride()}")
     return t.data_ptr()
 
 

@@ -140,3 +140,26 @@ def test_training_footprint_scales_expert_state_only():
     assert f64["expert_state"] == 64 * 3 * 1408 * 2048 * (2 + 2 + 12)
     assert abs(f64["activations"] - f8["activations"]) < 1e-3 * f64["activations"]
     assert f64["owner"] == f8["owner"]
+
+
+def test_binding_refuses_host_and_strided_tensors():
+    """The binding hands device addresses to the library: a host tensor, or a view whose elements are not dense,
+    is refused before any call is made."""
+    import torch
+    d = desc()
+    x = torch.zeros(256, 256)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        P.moe_route(d, x, FAKE, None, 1, FAKE, FAKE, FAKE, stream=0)
+
+    class StridedDeviceView:  # stands in for a non-contiguous GPU tensor without a GPU
+        is_cuda = True
+        shape = (256, 128)
+
+        def is_contiguous(self):
+            return False
+
+        def stride(self):
+            return (256, 2)
+
+    with pytest.raises(ValueError, match="contiguous"):
+        P.moe_route(d, StridedDeviceView(), FAKE, None, 1, FAKE, FAKE, FAKE, stream=0)
