@@ -38,6 +38,9 @@ def small_cases():
     C["E200_k8_d384"] = (LayerConfig("e200", T=512, d=384, f=256, E=200, k=8, seed=23), None)
     C["E128_f32"] = (LayerConfig("e128", T=256, d=256, f=128, E=128, k=2, dtype="f32", seed=24), None)
     C["E24_k3"] = (LayerConfig("e24", T=300, d=512, f=256, E=24, k=3, n_shared=1, seed=25), None)
+    # the largest supported shapes of the routing and of the tile plan: E = 256 experts, k = 8, and 511 groups
+    # (256 hosted + 255 shared experts), most of them with a handful of rows
+    C["E256_k8_511_groups"] = (LayerConfig("g511", T=64, d=128, f=128, E=256, k=8, n_shared=255, seed=31), None)
 
     def forced_empty(inp):
         inp.logit_bias[0, 3] = -1e4
