@@ -97,7 +97,7 @@ moe_status moe_route(const moe_desc* desc, const void* x, const void* w_router, 
                      int32_t bias_groups, float* logits, int32_t* topk_idx, float* topk_w, hipStream_t stream);
 
 /*
- * Dispatch, Alg. 3 ("Send h to the host of each selected expert"): a stable counting sort of
+ * Dispatch, Alg. 3 (each token's hidden state to the hosts of its selected experts): a stable counting sort of
  * the hosted slots by expert and a gather of their token rows.
  *   topk_idx    [T, k] int32 in
  *   x           [T, d] dtype in
@@ -201,7 +201,7 @@ typedef struct {
 } moe_opt;
 
 /*
- * "Update parameters of E_j" (Alg. 6, the host-side step after BackwardExpert) for every hosted
+ * The update of the expert parameters that ends the host's step in Alg. 6 (after BackwardExpert) for every hosted
  * routed expert and every shared expert, elementwise in fp32:
  *   SGD:    p <- p - lr * (g + weight_decay * p)
  *   AdamW:  p <- p * (1 - lr * weight_decay);  m <- beta1 m + (1 - beta1) g;  v <- beta2 v + (1 - beta2) g^2;

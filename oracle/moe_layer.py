@@ -12,7 +12,7 @@ Plain, slow and fp64. Every function follows the paper's statement of the layer:
   hidden state, runs ForwardExpert, and the owner forms sum_idx w_e[idx] * h^e_idx.
 * Expert passes, Alg. 6 (ForwardExpert / BackwardExpert): h^e = E_j(h); backprop through E_j.
   Each expert is a SwiGLU feed-forward block W_down (silu(W_gate h) * (W_up h)).
-* Backward, Alg. 5 (BackwardExperts) and Sec. 3.2 "Backward propagation": the host of an
+* Backward, Alg. 5 (BackwardExperts) and Sec. 3.2 (backward propagation): the host of an
   expert receives the gradient w.r.t. that expert's output and returns the gradient w.r.t.
   its input; the router (part of the owner's backbone) is differentiated by the data owner.
 * Expert sharding, Sec. 3.1 (2): a party hosts a shard of the global expert pool; here a
@@ -81,7 +81,7 @@ def gate_weights(logits, idx, renormalize=True):
     return w
 
 
-# ------------------------------------------------------------------ dispatch (Alg. 3, "Send h")
+# ------------------------------------------------------------------ dispatch (Alg. 3: hidden states to the experts' hosts)
 
 def permutation(idx, local_begin, local_count):
     """Group the assignment slots a = t*k + j of the hosted experts by expert.

@@ -1,6 +1,6 @@
 """Oracle of the expert parameter update — test infrastructure, not part of the product.
 
-Alg. 6 ends the host's expert step with "Update parameters of E_j" and leaves the optimiser open.
+Alg. 6 ends the host's expert step with an update of the expert's parameters and leaves the optimiser open.
 Two are offered, each written from its definition, in fp64 over the exact stored values:
 
 * SGD with weight decay added to the gradient: p <- p - lr * (g + wd * p).

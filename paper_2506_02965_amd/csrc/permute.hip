@@ -1,4 +1,4 @@
-// Dispatch of Alg. 3 ("Send h to the host of each selected expert") as a stable counting sort
+// Dispatch of Alg. 3 (each token's hidden state goes to the host of every expert it selected) as a stable counting sort
 // of the hosted assignment slots a = t*k + j by expert, plus the gather of their token rows;
 // and the hand-back of the input gradient (Sec. 3.2), summed per token.
 //

@@ -1,4 +1,4 @@
-// Expert parameter update ("Update parameters of E_j", Alg. 6): SGD or AdamW with decoupled weight
+// Expert parameter update (the step that closes the host's expert pass in Alg. 6): SGD or AdamW with decoupled weight
 // decay, elementwise in fp32 over the hosted and shared experts' w_gate, w_up and w_down.
 // Bandwidth-bound: each thread updates 8 consecutive parameters with 16-byte vector accesses.
 #include "pcmoe_internal.h"

@@ -245,6 +245,40 @@ def pin_dense_expert(ml):
     assert np.all(bwd["dW_router"] == 0)    # k = 1 renormalised: the gate weight is constantly 1
 
 
+def pin_hand_worked(ml):
+    """A two-token layer small enough to work out by hand (d = 2, E = 2, k = 1, f = 1, integer weights).
+
+    Token 0 = (1, 0) scores (2, 0) and goes to expert 0; token 1 = (0, 1) scores (0, 1) and goes to expert 1, each
+    with gate weight 1 (top-1, renormalised). With s1 = sigmoid(1), s2 = sigmoid(2):
+      expert 0: G = 1, U = 1, H = s1,          O = W_down0 H = ( s1, -s1)
+      expert 1: G = 2, U = 3, H = 2 s2 * 3,     O = W_down1 H = (2H, H)
+    Backward with dY = I: dO = dY rows; dH = W_down^T dO = 1 for both tokens;
+      dU = dH silu(G), dG = dH U s(G) (1 + G (1 - s(G)));
+      dx0 = (dG0 + dU0, dU0), dx1 = (0, 2 dG1 + 3 dU1); dW_down_e = dO_e H_e, dW_gate_e = dG_e x_e,
+      dW_up_e = dU_e x_e; dgate_t = <dY_t, O_t>; the router gradient is 0 (the weight is constantly 1)."""
+    import math
+    s1, s2 = 1 / (1 + math.exp(-1.0)), 1 / (1 + math.exp(-2.0))
+    cfg = LayerConfig("hand", T=2, d=2, f=1, E=2, k=1, dtype="f32")
+    inp = LayerInputs(cfg, x=np.array([[1.0, 0.0], [0.0, 1.0]]), dy=np.eye(2),
+                      w_router=np.array([[2.0, 0.0], [0.0, 1.0]]), logit_bias=None,
+                      w_gate=np.array([[[1.0, 0.0]], [[0.0, 2.0]]]), w_up=np.array([[[1.0, 1.0]], [[0.0, 3.0]]]),
+                      w_down=np.array([[[1.0], [-1.0]], [[2.0], [1.0]]]))
+    H0, H1 = s1, 2 * s2 * 3
+    dU0, dG0 = s1, 1 * s1 * (1 + (1 - s1))
+    dU1, dG1 = 2 * s2, 3 * s2 * (1 + 2 * (1 - s2))
+    fwd = ml.layer_forward(inp)
+    assert fwd["topk_idx"].reshape(-1).tolist() == [0, 1]
+    assert np.allclose(fwd["topk_w"].reshape(-1), [1.0, 1.0], rtol=0, atol=1e-15)
+    assert np.allclose(fwd["y"], [[H0, -H0], [2 * H1, H1]], rtol=1e-14, atol=0)
+    bwd = ml.layer_backward(inp, fwd, inp.dy)
+    assert np.allclose(bwd["dgate"].reshape(-1), [H0, H1], rtol=1e-14, atol=0)
+    assert np.allclose(bwd["dx"], [[dG0 + dU0, dU0], [0.0, 2 * dG1 + 3 * dU1]], rtol=1e-14, atol=1e-15)
+    assert np.allclose(bwd["dW_down"], [[[H0], [0.0]], [[0.0], [H1]]], rtol=1e-14, atol=1e-15)
+    assert np.allclose(bwd["dW_gate"], [[[dG0, 0.0]], [[0.0, dG1]]], rtol=1e-14, atol=1e-15)
+    assert np.allclose(bwd["dW_up"], [[[dU0, 0.0]], [[0.0, dU1]]], rtol=1e-14, atol=1e-15)
+    assert np.all(bwd["dW_router"] == 0)
+
+
 def pin_identical_experts(ml):
     """All routed experts share weights: renormalised gate weights sum to 1, so Y = FFN(x)."""
     cfg = LayerConfig("ident", T=64, d=16, f=24, E=6, k=3, dtype="f32", seed=5)
@@ -344,6 +378,10 @@ def test_dense_expert():
     pin_dense_expert(moe_layer)
 
 
+def test_hand_worked():
+    pin_hand_worked(moe_layer)
+
+
 def test_identical_experts():
     pin_identical_experts(moe_layer)
 
@@ -398,6 +436,7 @@ def test_planted_wrong_silu_derivative(monkeypatch):
     monkeypatch.setattr(moe_layer, "dsilu", lambda z: expit(z))          # drops the z*s*(1-s) term
     assert _fails(pin_finite_differences, moe_layer)
     assert _fails(pin_dense_torch, moe_layer)
+    assert _fails(pin_hand_worked, moe_layer)
 
 
 def test_planted_silu_on_up_projection(monkeypatch):
@@ -409,6 +448,7 @@ def test_planted_silu_on_up_projection(monkeypatch):
     monkeypatch.setattr(moe_layer, "expert_forward", bad_forward)
     assert _fails(pin_dense_torch, moe_layer)
     assert _fails(pin_brute_force, moe_layer)
+    assert _fails(pin_hand_worked, moe_layer)
 
 
 def test_planted_missing_renormalisation(monkeypatch):
@@ -460,3 +500,4 @@ def test_planted_transposed_down_projection(monkeypatch):
     monkeypatch.setattr(moe_layer, "expert_backward", bad_backward)
     assert _fails(pin_finite_differences, moe_layer)
     assert _fails(pin_euler_identities, moe_layer)
+    assert _fails(pin_hand_worked, moe_layer)
