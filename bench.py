@@ -114,8 +114,9 @@ def cpu_baseline(cfg, inp, min_seconds=10.0, max_seconds=30.0):
 
 def measure_expert_update(P, layer, w, steps):
     """The expert update (AdamW with an fp32 master copy) over the hosted experts, timed on its own
-    after the layer steps: HBM bytes per launch = parameters x (weight 2+2, gradient 2, master 4+4,
-    moments 8+8) for bf16 weights."""
+    after the layer steps: HBM bytes per launch = parameters x (weight written 2, gradient read 2, master
+    4+4, moments 8+8) for bf16 weights. With a master copy the stored weight is only written: the update
+    reads the fp32 master instead."""
     import torch
     layer.init_update_state(w, master=True)
     opt = P.make_opt(kind="adamw", lr=1e-4, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1)
@@ -133,7 +134,7 @@ def measure_expert_update(P, layer, w, steps):
     P.moe_kernel_timing_select(None)
     params = layer.opt_m.numel()
     es = w.w_gate.element_size()
-    per_param = 3 * es + 8 + 16           # weight read+write, gradient read; master and moments read+write
+    per_param = 2 * es + 8 + 16           # weight written, gradient read; master and moments read+write
     avg_s = ms / cnt / 1e3
     gbs = params * per_param / avg_s / 1e9
     return {"kernel": "expert_update", "optimizer": "adamw, fp32 master", "parameters": params,
