@@ -163,3 +163,25 @@ def test_binding_refuses_host_and_strided_tensors():
 
     with pytest.raises(ValueError, match="contiguous"):
         P.moe_route(d, StridedDeviceView(), FAKE, None, 1, FAKE, FAKE, FAKE, stream=0)
+
+
+def test_header_compiles_as_c(tmp_path):
+    """include/pcmoe.h is a C header: a C11 translation unit that includes it and uses its types and calls
+    compiles with no diagnostic from the header itself."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None or not os.path.isdir("/opt/rocm/include"):
+        pytest.skip("gcc or the ROCm headers are not available")
+    src = tmp_path / "abi_check.c"
+    src.write_text('#include "pcmoe.h"\n'
+                   "int main(void) {\n"
+                   "  moe_desc d = {0};\n"
+                   "  moe_opt o = {0};\n"
+                   "  (void)o;\n"
+                   "  return moe_route(&d, 0, 0, 0, 1, 0, 0, 0, 0) == MOE_OK ? 0 : (int)moe_status_string(MOE_OK)[0];\n"
+                   "}\n")
+    r = subprocess.run(["gcc", "-std=c11", "-Wall", "-Wextra", "-fsyntax-only", "-D__HIP_PLATFORM_AMD__",
+                        "-I/opt/rocm/include", "-I" + os.path.join(ROOT, "include"), str(src)],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stderr
+    assert "pcmoe.h" not in r.stderr, r.stderr
