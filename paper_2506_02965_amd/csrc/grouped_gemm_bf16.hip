@@ -10,8 +10,12 @@
 //   * operands whose K is the slow dimension (W_down / W_{gate,up} in the input gradients, both
 //     operands of the weight gradients) stay in their natural [k][mn] layout and are transposed on
 //     the way into registers by ds_read_b64_tr_b16 (two reads per MFMA operand);
-//   * four wavefronts (2 x 2) per workgroup, fp32 accumulators in AGPR/VGPRs, per-wave epilogue
-//     staged through LDS in fp32 and written as 16-byte chunks (SwiGLU and its adjoint fused).
+//   * 256 x 256 tiles with 16 wavefronts (4 x 4, 64 x 64 each) by default, 192 x 256 tiles with 8
+//     wavefronts for a single-round down projection, 128 x 128 tiles with 4 when a side is not a multiple
+//     of 256; fp32 accumulators, per-wave epilogue staged through LDS in fp32 and written as 16-byte
+//     chunks (SwiGLU and its adjoint fused);
+//   * tiles decoded on the device from a plan of m-tile prefixes (grouped_gemm.h); independent
+//     contractions of the backward share one launch (gemm_bf16_pair_kernel).
 #include "grouped_gemm.h"
 
 #include <cstdlib>
@@ -482,9 +486,9 @@ static hipError_t run2(const GemmArgs& a, long tiles, hipStream_t s, const char*
   return hipGetLastError();
 }
 
-// Tile shapes (BM x BN, LDS stages, wavefronts) instantiated for every contraction. Two wavefronts
-// per SIMD are what keep the MFMA pipes busy: 4-wave 128x128 tiles run two workgroups per CU,
-// the larger tiles use 8 wavefronts in one workgroup.
+// Tile shapes (BM x BN, LDS stages, wavefronts) instantiated for every contraction. The default is
+// 256 x 256 with 16 wavefronts (one workgroup per CU, four wavefronts per SIMD); 4-wavefront 128 x 128
+// tiles run two workgroups per CU. The other shapes are selectable for measurement (PCMOE_GEMM_TILES).
 // 192-row tiles (K-contiguous A only: the row-ragged contractions) serve a contraction whose 256-row grid is
 // one partial round of the chip.
 enum TileShape { T128x128s2 = 0, T256x128w8, T128x256w8, T256x256w8, T256x256k32, T256x128k32, T128x128k32,
