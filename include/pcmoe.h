@@ -27,10 +27,16 @@
  *   - Errors: a non-zero moe_status is returned and nothing is enqueued; arguments are
  *     checked before any launch. moe_last_error() gives a thread-local explanation.
  *     MOE_ERR_INVALID_ARGUMENT: null or misaligned pointer, k<1, k>E, bad shard range,
- *       bias_groups not dividing T, bad dtype. MOE_ERR_UNSUPPORTED: d_model or d_ff not a multiple of 128,
- *       E > 256, k > 8, T*k*d beyond int32 row indexing. MOE_ERR_WORKSPACE_TOO_SMALL: ws_bytes
- *       below moe_workspace_size(). MOE_ERR_HIP: a kernel launch failed.
+ *       local_count < 1 (a party hosts at least one routed expert), bias_groups not dividing T, bad dtype.
+ *     MOE_ERR_UNSUPPORTED: d_model or d_ff not a multiple of 128, E > 256, k > 8,
+ *       local_count + n_shared > 511, T*k beyond int32 slot indexing, T * max(d_model, 2*d_ff) * elem_bytes
+ *       >= 2^31 (one expert group's widest operand, addressed with 32-bit offsets), or
+ *       d_ff * d_model * elem_bytes >= 2^31 (one expert's weight matrix).
+ *     MOE_ERR_WORKSPACE_TOO_SMALL: ws_bytes below moe_workspace_size(). MOE_ERR_HIP: a kernel launch failed.
  *   - Calls are reentrant; concurrent calls must use distinct output and workspace buffers.
+ *   - Global state: the thread-local error string, and the per-kernel timing state of the measurement
+ *     calls at the end of this header (off unless moe_kernel_timing(1) is called; its events are created by
+ *     that call, never by a layer call).
  */
 #ifndef PCMOE_H
 #define PCMOE_H
@@ -225,7 +231,10 @@ moe_status moe_expert_update(const moe_desc* desc, const moe_opt* opt, void* w_g
                              float* v, hipStream_t stream);
 
 /* Per-kernel timing with HIP events recorded around every kernel launch on its own stream
- * (measurement aid; off by default). enable=1 clears the totals and starts recording. */
+ * (measurement aid; off by default). enable=1 clears the totals and starts recording; its first use creates
+ * a pool of 8192 HIP events and a table for 4096 launches, kept until the process ends (MOE_ERR_HIP if the
+ * events cannot be created). Layer calls take events from the pool and allocate nothing; launches beyond the
+ * pool go unrecorded and are reported as "(unrecorded)". enable=0 stops recording. */
 moe_status moe_kernel_timing(int enable);
 /* Restricts recording to the launches of one kernel (e.g. "gemm_bwd_dx"); NULL records all. */
 moe_status moe_kernel_timing_select(const char* kernel_name);

@@ -45,9 +45,11 @@ moe_status check_desc(const moe_desc* d) {
   if (d->local_count < 0 || d->local_begin < 0 || d->local_begin + d->local_count > d->n_experts)
     return fail(MOE_ERR_INVALID_ARGUMENT, "hosted range [%d, %d+%d) outside [0, %d)", d->local_begin,
                 d->local_begin, d->local_count, d->n_experts);
-  if (d->local_count + d->n_shared < 1 || d->n_shared < 0)
-    return fail(MOE_ERR_INVALID_ARGUMENT, "no expert to compute (local_count=%d n_shared=%d)", d->local_count,
-                d->n_shared);
+  if (d->n_shared < 0) return fail(MOE_ERR_INVALID_ARGUMENT, "n_shared=%d < 0", d->n_shared);
+  // A party hosts at least one routed expert: the dispatch, the combine and the grouped GEMMs all read the
+  // per-expert offsets that moe_permute produces for the hosted range.
+  if (d->local_count < 1)
+    return fail(MOE_ERR_INVALID_ARGUMENT, "local_count=%d: at least one hosted routed expert", d->local_count);
   if (d->renormalize != 0 && d->renormalize != 1)
     return fail(MOE_ERR_INVALID_ARGUMENT, "renormalize must be 0 or 1");
   if (d->top_k > 8) return fail(MOE_ERR_UNSUPPORTED, "top_k=%d > 8", d->top_k);
@@ -61,6 +63,17 @@ moe_status check_desc(const moe_desc* d) {
     return fail(MOE_ERR_UNSUPPORTED, "row space of %lld rows is too large", (long long)R);
   if ((int64_t)d->T * d->top_k >= ((int64_t)1 << 31) - 1024)
     return fail(MOE_ERR_UNSUPPORTED, "T*k too large for int32 slot indices");
+  // The grouped GEMMs address one group's operand rows and one expert's weight matrix through 32-bit buffer
+  // ranges and 32-bit lane offsets. A group holds at most T rows (a token selects an expert once; a shared
+  // expert takes every token), and its widest row is max(d_model, 2 d_ff) elements (x / dY rows, or the
+  // G|U and dG|dU rows).
+  const int64_t es = d->dtype == MOE_BF16 ? 2 : 4;
+  const int64_t row_bytes = (int64_t)(d->d_model > 2 * d->d_ff ? d->d_model : 2 * d->d_ff) * es;
+  if ((int64_t)d->T * row_bytes >= ((int64_t)1 << 31))
+    return fail(MOE_ERR_UNSUPPORTED, "T=%d rows of %lld bytes exceed the 2 GiB extent of one operand group", d->T,
+                (long long)row_bytes);
+  if ((int64_t)d->d_ff * d->d_model * es >= ((int64_t)1 << 31))
+    return fail(MOE_ERR_UNSUPPORTED, "one expert's %d x %d weight matrix exceeds 2 GiB", d->d_ff, d->d_model);
   return MOE_OK;
 }
 
@@ -81,16 +94,23 @@ moe_status check_desc(const moe_desc* d) {
   } while (0)
 
 // ------------------------------------------------------------------ per-kernel timing
+// The library's one global besides the thread-local error string: a measurement aid, off by default. Its event
+// pool and record table are created by moe_kernel_timing(1) (the only call that creates anything); the layer calls
+// then take events from the pool and append to the preallocated table, so they never allocate, timing on or off.
+// When the pool is spent, further launches go unrecorded (counted in `dropped`).
+constexpr size_t kTimingPairs = 4096;  // event pairs in the pool: launches recorded between two enables
 struct TimingState {
   std::mutex mu;
   std::atomic<bool> on{false};  // read without the lock on every launch (the common case: timing off)
   std::string only;  // record only launches with this name (empty: all)
   struct Rec {
-    std::string name;
+    const char* name;  // a launcher's string literal
     hipEvent_t a, b;
   };
-  std::vector<Rec> recs;
-  std::vector<hipEvent_t> pool;
+  std::vector<Rec> recs;         // capacity kTimingPairs, reserved once
+  std::vector<hipEvent_t> pool;  // 2 * kTimingPairs events, created once
+  size_t used = 0;               // pairs handed out since the last enable
+  size_t dropped = 0;
 };
 TimingState& timing() {
   static TimingState* t = new TimingState();
@@ -106,15 +126,14 @@ KernelTimer::KernelTimer(const char* n, hipStream_t s) : name(n), stream(s), slo
   std::lock_guard<std::mutex> lk(ts.mu);
   if (!ts.on.load(std::memory_order_relaxed)) return;
   if (!ts.only.empty() && ts.only != n) return;
-  hipEvent_t a = nullptr, b = nullptr;
-  if (ts.pool.size() >= 2) {
-    a = ts.pool.back(); ts.pool.pop_back();
-    b = ts.pool.back(); ts.pool.pop_back();
-  } else {
-    if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) return;
+  if (ts.used >= kTimingPairs || 2 * ts.used + 1 >= ts.pool.size()) {
+    ++ts.dropped;
+    return;
   }
+  hipEvent_t a = ts.pool[2 * ts.used], b = ts.pool[2 * ts.used + 1];
+  ++ts.used;
   hipEventRecord(a, s);
-  ts.recs.push_back({std::string(n), a, b});
+  ts.recs.push_back({n, a, b});  // within the reserved capacity
   slot = (void*)(uintptr_t)ts.recs.size();
 }
 KernelTimer::~KernelTimer() {
@@ -171,7 +190,6 @@ moe_status moe_permute(const moe_desc* d, const int32_t* topk_idx, const void* x
                        hipStream_t stream) {
   moe_status st = check_desc(d);
   if (st) return st;
-  if (d->local_count < 1) return fail(MOE_ERR_INVALID_ARGUMENT, "moe_permute needs local_count >= 1");
   NEED(topk_idx); NEED(x); NEED(counts); NEED(offsets); NEED(row_to_slot); NEED(slot_to_row); NEED(x_perm);
   NEED_WS(ws_bytes, permute_ws_bytes(*d));
   return hip_status(launch_permute(*d, topk_idx, x, counts, offsets, row_to_slot, slot_to_row, x_perm, ws, stream),
@@ -184,7 +202,7 @@ moe_status moe_expert_ffn_fwd(const moe_desc* d, const void* x, const void* x_pe
   moe_status st = check_desc(d);
   if (st) return st;
   if (d->n_shared > 0) NEED(x);
-  if (d->local_count > 0) { NEED(x_perm); NEED(offsets); }
+  NEED(x_perm); NEED(offsets);
   NEED(w_gate); NEED(w_up); NEED(w_down); NEED(y_perm); NEED(saved);
   NEED_WS(ws_bytes, ffn_fwd_ws_bytes(*d));
   return hip_status(launch_ffn_fwd(*d, x, x_perm, offsets, w_gate, w_up, w_down, y_perm, saved, ws, stream),
@@ -215,7 +233,7 @@ moe_status moe_expert_ffn_bwd(const moe_desc* d, const void* x, const void* x_pe
   moe_status st = check_desc(d);
   if (st) return st;
   if (d->n_shared > 0) { NEED(x); NEED(dy); }
-  if (d->local_count > 0) { NEED(x_perm); NEED(dy_perm); NEED(offsets); }
+  NEED(x_perm); NEED(dy_perm); NEED(offsets);
   NEED(w_gate); NEED(w_up); NEED(w_down); NEED(saved); NEED(dx_perm); NEED(dw_gate); NEED(dw_up); NEED(dw_down);
   NEED_WS(ws_bytes, ffn_bwd_ws_bytes(*d));
   return hip_status(launch_ffn_bwd(*d, x, x_perm, dy, dy_perm, offsets, w_gate, w_up, w_down, saved, dx_perm,
@@ -279,11 +297,20 @@ moe_status moe_expert_update(const moe_desc* d, const moe_opt* opt, void* w_gate
 moe_status moe_kernel_timing(int enable) {
   TimingState& ts = timing();
   std::lock_guard<std::mutex> lk(ts.mu);
-  for (auto& r : ts.recs) {
-    ts.pool.push_back(r.a);
-    ts.pool.push_back(r.b);
+  if (enable && ts.pool.size() < 2 * kTimingPairs) {
+    ts.recs.reserve(kTimingPairs);
+    while (ts.pool.size() < 2 * kTimingPairs) {
+      hipEvent_t e = nullptr;
+      if (hipError_t err = hipEventCreate(&e); err != hipSuccess) {
+        ts.on.store(false, std::memory_order_release);
+        return hip_status(err, "moe_kernel_timing");
+      }
+      ts.pool.push_back(e);
+    }
   }
   ts.recs.clear();
+  ts.used = 0;
+  ts.dropped = 0;
   ts.on.store(enable != 0, std::memory_order_release);
   return MOE_OK;
 }
@@ -300,6 +327,10 @@ size_t moe_kernel_timing_report(char* buf, size_t n) {
   std::lock_guard<std::mutex> lk(ts.mu);
   std::map<std::string, std::pair<long, double>> agg;
   std::vector<std::string> order;
+  if (ts.dropped) {
+    order.push_back("(unrecorded)");
+    agg["(unrecorded)"] = {(long)ts.dropped, 0.0};
+  }
   for (auto& r : ts.recs) {
     float ms = 0.f;
     if (hipEventSynchronize(r.b) != hipSuccess || hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) continue;

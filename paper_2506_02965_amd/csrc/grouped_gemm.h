@@ -79,7 +79,7 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs& p, int bid, TileIdx&
       if (RAGGED && i <= G) pre[s] = p.mt_prefix[i];
       if (split && i <= G) tl[s] = p.mt_tail[i];
       if (!RAGGED && p.order && i <= G) ord[s] = p.order[i];
-      if (i <= p.Eloc) off[s] = p.offsets[i];
+      if (p.Eloc > 0 && i <= p.Eloc) off[s] = p.offsets[i];
     }
   }
   int total;

@@ -62,12 +62,34 @@ FAKE = 0x1000  # never dereferenced: every call below fails validation first
     (dict(d_ff=100), P.MOE_ERR_UNSUPPORTED),
     (dict(n_experts=300), P.MOE_ERR_UNSUPPORTED),
     (dict(dtype="bf16", renormalize=True, T=0), P.MOE_ERR_INVALID_ARGUMENT),
+    # a shard without a hosted routed expert (shared experts only) is refused: there are no offsets to read
+    (dict(local_begin=0, local_count=0, n_shared=1), P.MOE_ERR_INVALID_ARGUMENT),
+    # 32-bit operand extents of the grouped GEMMs: one group's dG|dU rows (T * 2 d_ff * 2 bytes) ...
+    (dict(T=65536, d_model=128, d_ff=16384, n_experts=1, top_k=1, dtype="bf16"), P.MOE_ERR_UNSUPPORTED),
+    (dict(T=131072, d_model=4096, d_ff=14336, n_experts=8, top_k=2, dtype="bf16"), P.MOE_ERR_UNSUPPORTED),
+    # ... one group's x rows when d_model > 2 d_ff, and one expert's weight matrix
+    (dict(T=262144, d_model=4096, d_ff=128, n_experts=8, top_k=2, dtype="bf16"), P.MOE_ERR_UNSUPPORTED),
+    (dict(T=64, d_model=32768, d_ff=32768, n_experts=8, top_k=2, dtype="bf16"), P.MOE_ERR_UNSUPPORTED),
 ])
 def test_descriptor_validation(kw, status):
     d = desc(**kw)
     with pytest.raises(P.MoeError) as ei:
         P.moe_combine(d, FAKE, FAKE, FAKE, FAKE, stream=0)
     assert ei.value.status == status
+
+
+def test_extent_limits_admit_the_workloads():
+    """The 2 GiB operand-extent bound leaves every benchmark workload, and the shapes just below it, accepted."""
+    from paper_2506_02965_amd.synth import CONFIGS
+    for c in CONFIGS.values():
+        d = P.make_desc(c.T, c.d, c.f, c.E, c.k, c.local_begin, c.n_local, c.n_shared, c.renormalize, c.dtype)
+        assert P.moe_workspace_size(d, P.MOE_WS_FFN_SAVED) > 0, c.name
+    # largest T for d_ff = 14336 in bf16: T * 2 * 14336 * 2 < 2^31
+    t_max = ((1 << 31) - 1) // (4 * 14336)
+    ok = desc(T=t_max, d_model=4096, d_ff=14336, n_experts=8, top_k=2, dtype="bf16")
+    assert P.moe_workspace_size(ok, P.MOE_WS_FFN_SAVED) > 0
+    over = desc(T=t_max + 1, d_model=4096, d_ff=14336, n_experts=8, top_k=2, dtype="bf16")
+    assert P.moe_workspace_size(over, P.MOE_WS_FFN_SAVED) == 0
 
 
 def test_null_pointers_and_workspace():
