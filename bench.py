@@ -4,8 +4,9 @@
 
 One step is one pass of the whole layer over one batch of resident synthetic inputs:
 route -> permute -> expert FFN forward -> combine -> combine backward -> expert FFN backward
--> router backward -> unpermute. The workload is the bf16 layer T=4096, d=1024, f=2816,
-E=16 SwiGLU experts, top-2 (seeded inputs, weights ~ N(0, 1/fan_in)).
+-> router backward -> unpermute. The default workload is the largest one, the bf16 layer T=8192,
+d=4096, f=14336, E=8 SwiGLU experts, top-2 (seeded inputs, weights ~ N(0, 1/fan_in)); --workload
+selects another.
 
 Prints ONE JSON line: the layer's algorithmic TFLOP/s (6*d*f per routed-or-shared row forward,
 12*d*f backward, 2*T*d*E router forward, 4*T*d*E router backward), tokens/s, the roofline of the
@@ -85,31 +86,77 @@ def layer_flops(cfg, n_routed_rows, backward=True):
     return fl
 
 
-def cpu_baseline(cfg, inp, min_seconds=10.0, max_seconds=30.0):
-    """The CPU oracle (fp64 numpy) on this host's cores, timed on a bounded sample of the workload:
-    whole forward + backward passes of the layer, repeated until about min_seconds of CPU work
-    (first pass always counted; no new pass starts beyond max_seconds)."""
-    from oracle import moe_layer as O
+def host_info():
+    """What the CPU baseline ran on: the cores this process may use, the CPU model, the BLAS library numpy calls
+    and its thread count (the threads the oracle's matrix products actually use)."""
+    import numpy as np
+    np.ones((64, 64)) @ np.ones((64, 64))             # loads the BLAS so that its thread pool is reported
+    blas, threads = "unknown", None
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+        pools = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if pools:
+            blas = f"{pools[0].get('internal_api')} {pools[0].get('version')} ({pools[0].get('threading_layer')})"
+            threads = max(int(i.get("num_threads", 1)) for i in pools)
     except Exception:
-        threads = os.cpu_count() or 1
-    n_pass, total, n_rows = 0, 0.0, 0
-    while True:
-        t0 = time.perf_counter()
-        fwd = O.layer_forward(inp)
-        O.layer_backward(inp, fwd, inp.dy)
-        total += time.perf_counter() - t0
-        n_pass += 1
-        n_rows = len(fwd["row_to_slot"])
-        if total >= min_seconds or total * (n_pass + 1) / n_pass > max_seconds:
+        pass
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    avail = len(os.sched_getaffinity(0))
+    return {"cores_available": avail, "cpu_model": model, "blas": blas, "blas_threads": threads or avail}
+
+
+def cpu_baseline(cfg, inp, min_seconds=10.0, max_seconds=30.0):
+    """The CPU oracle (fp64 numpy) on this host's cores, timed on a bounded sample of the workload: the oracle's
+    routing and dispatch of every token (scores, top-k, gate weights, the permutation), then its forward and
+    backward of one expert at a time over that expert's rows (hosted experts in order, then shared ones), the
+    per-expert steps of the whole-layer oracle, until about min_seconds of CPU work (at least one expert; no
+    expert starts that would end past max_seconds by the last one's time). Throughput = the algorithmic FLOPs
+    of the sampled work (router forward 2*T*d*E, 18*d*f per expert row) / its time."""
+    import numpy as np
+    from oracle import moe_layer as O
+    info = host_info()
+    T, d, f, E, k = cfg.T, cfg.d, cfg.f, cfg.E, cfg.k
+    t0 = time.perf_counter()
+    L64 = O.router_logits(inp.x, inp.w_router, inp.logit_bias, cfg.bias_groups)
+    idx = O.topk_indices(O.selection_logits(L64), k)
+    w = O.gate_weights(L64, idx, renormalize=cfg.renormalize)
+    counts, offsets, r2s, s2r = O.permutation(idx, cfg.local_begin, cfg.n_local)
+    flops = 2.0 * T * d * E
+    elapsed = time.perf_counter() - t0
+    x64, dy64, wflat = np.asarray(inp.x, np.float64), np.asarray(inp.dy, np.float64), w.reshape(-1)
+    done, rows_done, last = 0, 0, 0.0
+    for g in range(cfg.n_groups):
+        if done and (elapsed >= min_seconds or elapsed + last > max_seconds):
             break
-    dt = total / n_pass
-    fl = layer_flops(cfg, n_rows, True)
-    return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{n_pass} whole fwd+bwd pass(es) of the workload ({cfg.T} tokens), fp64 numpy, "
-                      f"{total:.1f} s in total", "tokens_per_s": round(cfg.T / dt, 2), "seconds_per_pass": round(dt, 3)}
+        t1 = time.perf_counter()
+        if g < cfg.n_local:
+            rr = r2s[offsets[g]:offsets[g + 1]]
+            tok = rr // k
+            h, dO = x64[tok], wflat[rr][:, None] * dy64[tok]
+        else:
+            h, dO = x64, dy64
+        if len(h):
+            G, U, Hd, _ = O.expert_forward(h, inp.w_gate[g], inp.w_up[g], inp.w_down[g])
+            O.expert_backward(h, inp.w_gate[g], inp.w_up[g], inp.w_down[g], G, U, Hd, dO)
+        last = time.perf_counter() - t1
+        elapsed += last
+        flops += 18.0 * d * f * len(h)
+        rows_done += len(h)
+        done += 1
+    out = {"value": flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": int(info["blas_threads"]), "kind": "oracle",
+           "sample": f"routing and dispatch of all {T} tokens, then forward + backward of {done} of the "
+                     f"{cfg.n_groups} experts ({rows_done} expert rows), fp64 numpy, {elapsed:.1f} s",
+           "sample_seconds": round(elapsed, 2), "sample_gflop": round(flops / 1e9, 1)}
+    out.update(info)
+    return out
 
 
 def measure_expert_update(P, layer, w, steps):
@@ -218,6 +265,14 @@ def memory_amortisation(P, parties=(1, 2, 4, 8)):
             "data": "synthetic", "rows": rows}
 
 
+DEFAULT_WORKLOAD = "bf16_T8192_d4096_f14336_E8_k2"
+
+
+def progress(msg):
+    """A progress line on stderr (stdout carries only the JSON line)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def pick_workload(key: str):
     from paper_2506_02965_amd.synth import CONFIGS
     for i, c in CONFIGS.items():
@@ -232,10 +287,11 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     # The first ~60 steps (~50 ms) of a fresh process run up to 7% slower than the steady state that follows;
-    # the default warm-up covers them.
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=100)
-    ap.add_argument("--workload", "--config", dest="workload", default="bf16_T4096_d1024_f2816_E16_k2",
+    # the warm-up runs at least --warmup steps and at least --min-warmup-seconds.
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--min-warmup-seconds", type=float, default=2.0)
+    ap.add_argument("--workload", "--config", dest="workload", default=DEFAULT_WORKLOAD,
                     help="workload name (" + ", ".join(c.name for c in WORKLOADS) + ") or its position 1-5 in that list")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--memory", action="store_true",
@@ -268,21 +324,28 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     cfg = pick_workload(args.workload)
+    progress(f"workload {cfg.name}: drawing the inputs")
     inp = make_inputs(cfg, with_dy=True)
     w = upload(inp, device="cuda")
     layer = MoELayer(cfg, backward=True)
+    progress("inputs resident on the GPU; warm-up")
 
     def step():
         layer.forward(w)
         layer.backward(w)
 
-    for _ in range(max(args.warmup - 2, 0)):
+    warm_steps, t_warm = 0, time.perf_counter()
+    while warm_steps < max(args.warmup - 2, 0) or time.perf_counter() - t_warm < args.min_warmup_seconds:
         step()
+        warm_steps += 1
+        if warm_steps % 8 == 0:
+            torch.cuda.synchronize()   # the host stays at most a few steps ahead, so the clock measures the GPU
     torch.cuda.synchronize()
+    warm_steps += 2
     n_routed = layer.n_local_rows()
     # the last two warm-up steps record every kernel to find the dominant one (untimed)
     P.moe_kernel_timing(True)
-    for _ in range(min(args.warmup, 2)):
+    for _ in range(2):
         step()
     torch.cuda.synchronize()
     kt_all = P.moe_kernel_timing_report()
@@ -307,7 +370,7 @@ def main():
     rows = n_routed + cfg.n_shared * cfg.T
     dom_cnt, dom_ms = kt[dom_name]
     dom_avg_s = dom_ms / dom_cnt / 1e3
-    nw = min(args.warmup, 2)
+    nw = 2
     kernels = {k: {"launches_per_step": c / nw, "avg_us": ms / c * 1e3} for k, (c, ms) in kt_all.items()}
     if dom_name in GEMM_FLOPS_PER_ROW_DF:
         per_launch = GEMM_FLOPS_PER_ROW_DF[dom_name] * cfg.d * cfg.f * rows
@@ -327,6 +390,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "warmup_steps_run": warm_steps,
         "ms_per_step": round(dt * 1e3, 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -346,6 +410,7 @@ def main():
     }
     out["expert_update"] = measure_expert_update(P, layer, w, args.steps)
     if not args.no_cpu_baseline:
+        progress("GPU steps done; timing the CPU oracle on a sample")
         out["cpu_baseline"] = cpu_baseline(cfg, inp)
     print(json.dumps(out), flush=True)
 

@@ -252,69 +252,69 @@ def router_logit_grad(logits, idx, w, dgate, renormalize=True):
     return dL
 
 
-# ---------------------------------------------------- per-token / per-row pieces for big shapes
+# ------------------------------------------------------ the whole layer one expert group at a time
 
-def token_route(inp, tokens):
-    """Routing of a subset of tokens only (scores, selection, gate weights)."""
+def layer_streamed(inp, dy=None):
+    """The same layer as layer_forward + layer_backward (Alg. 7, Alg. 3, Alg. 6, Alg. 5 and the router adjoint),
+    evaluated one expert group at a time so that no array spans the whole row space: for large shapes whose
+    per-row intermediates (G, U, H and their gradients over every routed row) do not fit in host memory at once.
+
+    A generator. It yields, in this order:
+      ("routing", dict(logits64, logits, topk_idx, topk_w, counts, offsets, row_to_slot, slot_to_row));
+      ("group", g, dict(rows, tokens, O, and with dy: dO, dxp, dW_gate, dW_up, dW_down)) for every hosted
+        routed expert g < n_local with at least one row (rows = its row-space indices, tokens = their tokens),
+        then every shared expert (rows T*k + s*T + t for all tokens t);
+      ("tokens", dict(y, and with dy: dgate, dx_experts, dx, and with the router adjoint: dlogits, dW_router)).
+    Each group's forward and backward are those of expert_forward / expert_backward on its rows; the token
+    outputs accumulate the groups' contributions (the owner-side combine of Alg. 3 and its adjoint)."""
     cfg = inp.cfg
-    x = f64(inp.x[tokens])
-    L = x @ f64(inp.w_router).T
-    if inp.logit_bias is not None:
-        group = np.asarray(tokens) // (cfg.T // cfg.bias_groups)
-        L = L + f64(inp.logit_bias)[group]
-    L32 = selection_logits(L)
-    idx = topk_indices(L32, cfg.k)
-    return L, L32, idx, gate_weights(L, idx, renormalize=cfg.renormalize)
-
-
-def token_forward_backward(inp, tokens, dy_rows=None):
-    """Y (and, with dY given, dgate and the expert part of dX) for a subset of tokens.
-
-    Each token's routed experts and the shared experts are evaluated on that token's row
-    alone, exactly as the whole-layer definition does for it (grouped by expert so that each
-    expert's weights are converted once)."""
-    cfg = inp.cfg
-    Eloc, S, k = cfg.n_local, cfg.n_shared, cfg.k
-    tokens = np.asarray(tokens)
-    _, L32, idx, w = token_route(inp, tokens)
-    x = f64(inp.x[tokens])
-    n = len(tokens)
-    Y = np.zeros((n, cfg.d))
-    dgate = np.zeros((n, k))
-    dx = np.zeros((n, cfg.d))
-    dyr = None if dy_rows is None else f64(dy_rows)
+    T, k, d = cfg.T, cfg.k, cfg.d
+    Eloc, S = cfg.n_local, cfg.n_shared
+    x = f64(inp.x)
+    L64 = router_logits(x, inp.w_router, inp.logit_bias, cfg.bias_groups)
+    L32 = selection_logits(L64)
+    idx = topk_indices(L32, k)
+    w = gate_weights(L64, idx, renormalize=cfg.renormalize)
+    counts, offsets, row_to_slot, slot_to_row = permutation(idx, cfg.local_begin, Eloc)
+    yield ("routing", dict(logits64=L64, logits=L32, topk_idx=idx, topk_w=w, counts=counts, offsets=offsets,
+                           row_to_slot=row_to_slot, slot_to_row=slot_to_row))
+    dyv = None if dy is None else f64(dy)
+    wflat = w.reshape(-1)
+    Y = np.zeros((T, d))
+    dgate = np.zeros((T, k))
+    dx = np.zeros((T, d))
     for g in range(Eloc + S):
         if g < Eloc:
-            hit = np.argwhere(idx == cfg.local_begin + g)      # (token position, slot j)
-            if hit.size == 0:
+            rows = np.arange(offsets[g], offsets[g + 1])
+            if rows.size == 0:
                 continue
-            rows, slots = hit[:, 0], hit[:, 1]
-            wj = w[rows, slots][:, None]
+            slots = row_to_slot[rows]
+            tokens = slots // k
+            wj = wflat[slots][:, None]                # gate weight of each row's slot
         else:
-            rows, slots = np.arange(n), None
-            wj = np.ones((n, 1))
-        G, U, Hd, O = expert_forward(x[rows], inp.w_gate[g], inp.w_up[g], inp.w_down[g])
-        np.add.at(Y, rows, wj * O)
-        if dyr is not None:
-            b = expert_backward(x[rows], inp.w_gate[g], inp.w_up[g], inp.w_down[g], G, U, Hd, wj * dyr[rows])
-            np.add.at(dx, rows, b["dh"])
+            s = g - Eloc
+            tokens = np.arange(T)
+            rows = T * k + s * T + tokens
+            slots = None
+            wj = np.ones((T, 1))                      # shared experts: always active, weight 1
+        h = x[tokens]
+        G, U, Hid, O = expert_forward(h, inp.w_gate[g], inp.w_up[g], inp.w_down[g])
+        Y[tokens] += wj * O                           # a token meets each expert at most once
+        out = dict(rows=rows, tokens=tokens, O=O)
+        if dyv is not None:
+            dO = wj * dyv[tokens]
+            b = expert_backward(h, inp.w_gate[g], inp.w_up[g], inp.w_down[g], G, U, Hid, dO)
+            dx[tokens] += b["dh"]
             if slots is not None:
-                dgate[rows, slots] = (dyr[rows] * O).sum(axis=1)
-    return dict(y=Y, dgate=dgate, dx_experts=dx, topk_idx=idx, topk_w=w, logits=L32)
-
-
-def expert_wgrad_slices(h, dO, w_gate, w_up, w_down, rows_ff, cols_ff):
-    """Selected rows of dW_gate / dW_up (inner units rows_ff) and columns of dW_down (inner units
-    cols_ff) of one expert, without forming its full backward: each needs only the inner units
-    it names (Alg. 6 backward restricted to those units)."""
-    h, dO = f64(h), f64(dO)
-    wg, wu, wd = f64(w_gate), f64(w_up), f64(w_down)
-    rows_ff, cols_ff = np.asarray(rows_ff), np.asarray(cols_ff)
-    G = h @ wg[rows_ff].T
-    U = h @ wu[rows_ff].T
-    dHid = dO @ wd[:, rows_ff]
-    dG = dHid * U * dsilu(G)
-    dU = dHid * silu(G)
-    Gc = h @ wg[cols_ff].T
-    Hc = silu(Gc) * (h @ wu[cols_ff].T)
-    return dict(dW_gate_rows=dG.T @ h, dW_up_rows=dU.T @ h, dW_down_cols=dO.T @ Hc)
+                dgate[tokens, slots % k] = np.einsum("td,td->t", dyv[tokens], O)
+            out.update(dO=dO, dxp=b["dh"], dW_gate=b["dW_gate"], dW_up=b["dW_up"], dW_down=b["dW_down"])
+        yield ("group", g, out)
+    tok = dict(y=Y)
+    if dyv is not None:
+        tok.update(dgate=dgate, dx_experts=dx.copy())
+        if cfg.router_backward:
+            dL = router_logit_grad(L64, idx, w, dgate, cfg.renormalize)
+            tok.update(dlogits=dL, dW_router=dL.T @ x)
+            dx = dx + dL @ f64(inp.w_router)
+        tok["dx"] = dx
+    yield ("tokens", tok)

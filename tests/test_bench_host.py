@@ -68,3 +68,28 @@ def test_workloads_by_name_and_position():
         assert bench.pick_workload(str(i)) is c
     with pytest.raises(SystemExit):
         bench.pick_workload("no_such_workload")
+
+
+def test_default_workload_is_the_largest():
+    """The headline runs on the layer with the most work per step (T=8192, d=4096, f=14336, E=8, top-2)."""
+    big = max(CONFIGS.values(), key=lambda c: c.T * c.k * c.d * c.f)
+    assert bench.DEFAULT_WORKLOAD == big.name == CONFIGS[4].name
+
+
+def test_host_info_fields():
+    info = bench.host_info()
+    assert info["cores_available"] == len(os.sched_getaffinity(0))
+    assert info["blas_threads"] >= 1 and isinstance(info["cpu_model"], str) and info["blas"]
+
+
+def test_cpu_baseline_sample_is_bounded():
+    """The oracle baseline on a small layer: routing of every token plus whole experts, stopping once the
+    time bound is met (here at once: one expert), with the FLOPs of exactly the sampled rows."""
+    from paper_2506_02965_amd.synth import make_inputs
+    cfg = LayerConfig("cb", T=64, d=128, f=128, E=4, k=2, seed=3)
+    inp = make_inputs(cfg, with_dy=True)
+    out = bench.cpu_baseline(cfg, inp, min_seconds=0.0, max_seconds=60.0)
+    assert out["kind"] == "oracle" and out["unit"] == "TFLOP/s" and out["value"] > 0
+    assert "1 of the 4 experts" in out["sample"]
+    rows = int(out["sample"].split("(")[1].split(" ")[0])
+    assert abs(out["sample_gflop"] * 1e9 - (2 * 64 * 128 * 4 + 18 * 128 * 128 * rows)) < 1e8

@@ -14,7 +14,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def test_bench_json_line():
     print("[bench] short run of bench.py", flush=True)
     r = subprocess.run([sys.executable, "-u", os.path.join(ROOT, "bench.py"), "--steps", "3", "--warmup", "3",
-                        "--no-cpu-baseline"], capture_output=True, text=True, timeout=110)
+                        "--min-warmup-seconds", "0.2", "--no-cpu-baseline", "--workload",
+                        "bf16_T4096_d1024_f2816_E16_k2"], capture_output=True, text=True, timeout=110)
     assert r.returncode == 0, r.stderr[-2000:]
     lines = [l for l in r.stdout.splitlines() if l.strip()]
     assert len(lines) == 1, r.stdout
@@ -22,7 +23,7 @@ def test_bench_json_line():
     for key in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better", "scaling",
                 "vs_baseline", "dtype", "data", "config", "roofline"):
         assert key in out, key
-    assert out["n_gpus"] == 1 and out["steps"] == 3 and out["warmup"] == 3
+    assert out["n_gpus"] == 1 and out["steps"] == 3 and out["warmup"] == 3 and out["warmup_steps_run"] >= 3
     assert out["value"] > 0 and out["ms_per_step"] > 0 and out["dtype"] == "bf16"
     assert out["config"]["workload"] == "bf16_T4096_d1024_f2816_E16_k2"
     roof = out["roofline"]

@@ -394,32 +394,63 @@ def test_shards_sum_to_layer():
     pin_shards_sum_to_layer(moe_layer)
 
 
-def test_token_pieces_match_layer():
-    """The per-token evaluation used for large shapes agrees with the whole-layer oracle."""
-    cfg = LayerConfig("tok", T=48, d=16, f=24, E=8, k=3, n_shared=1, dtype="f32", bias="zipf", seed=17)
+def _streamed(inp):
+    out = {"groups": {}}
+    for item in moe_layer.layer_streamed(inp, inp.dy):
+        if item[0] == "group":
+            out["groups"][item[1]] = item[2]
+        else:
+            out[item[0]] = item[1]
+    return out
+
+
+@pytest.mark.parametrize("kw", [
+    dict(T=48, d=16, f=24, E=8, k=3, n_shared=1, bias="zipf", seed=17),            # router adjoint + shared
+    dict(T=64, d=16, f=24, E=8, k=2, local_begin=2, local_count=4, router_backward=False, bias="party",
+         parties=4, seed=18),                                                          # a party's shard
+    dict(T=40, d=8, f=16, E=4, k=2, renormalize=False, seed=19),                       # paper-literal gating
+])
+def test_layer_streamed_matches_layer(kw):
+    """The one-group-at-a-time evaluation used for the largest shapes gives every output of the whole-layer
+    oracle: routing and permutation exactly, the row-space rows of each group, each expert's weight gradients,
+    and the token outputs."""
+    cfg = LayerConfig("stream", dtype="f32", **kw)
     inp = make_inputs(cfg, with_dy=True)
     fwd = moe_layer.layer_forward(inp)
     bwd = moe_layer.layer_backward(inp, fwd, inp.dy)
-    toks = np.array([0, 5, 17, 47])
-    tp = moe_layer.token_forward_backward(inp, toks, inp.dy[toks])
-    assert np.array_equal(tp["topk_idx"], fwd["topk_idx"][toks])
-    assert rel(tp["y"], fwd["y"][toks]) < 1e-12
-    assert rel(tp["dgate"], bwd["dgate"][toks]) < 1e-12
-    assert rel(tp["dx_experts"], bwd["dx_experts"][toks]) < 1e-12
-
-
-def test_wgrad_slices_match_layer():
-    cfg = LayerConfig("sl", T=64, d=16, f=24, E=4, k=2, dtype="f32", seed=19)
-    inp = make_inputs(cfg, with_dy=True)
-    fwd = moe_layer.layer_forward(inp)
-    bwd = moe_layer.layer_backward(inp, fwd, inp.dy)
-    for e in range(cfg.n_local):
-        r0, r1 = fwd["offsets"][e], fwd["offsets"][e + 1]
-        sl = moe_layer.expert_wgrad_slices(fwd["xp"][r0:r1], bwd["dO"][r0:r1], inp.w_gate[e], inp.w_up[e],
-                                           inp.w_down[e], [0, 5, 23], [1, 7])
-        assert rel(sl["dW_gate_rows"], bwd["dW_gate"][e][[0, 5, 23]]) < 1e-12
-        assert rel(sl["dW_up_rows"], bwd["dW_up"][e][[0, 5, 23]]) < 1e-12
-        assert rel(sl["dW_down_cols"], bwd["dW_down"][e][:, [1, 7]]) < 1e-12
+    st = _streamed(inp)
+    for key in ("topk_idx", "counts", "offsets", "row_to_slot", "slot_to_row"):
+        assert np.array_equal(st["routing"][key], fwd[key]), key
+    assert np.array_equal(st["routing"]["topk_w"], fwd["topk_w"])
+    N, TK = len(fwd["row_to_slot"]), cfg.T * cfg.k
+    seen = []
+    for g, grp in st["groups"].items():
+        rows = grp["rows"]
+        if g < cfg.n_local:
+            assert rows.min() >= 0 and rows.max() < N
+            assert rel(grp["O"], fwd["O"][rows]) < 1e-12
+            assert rel(grp["dO"], bwd["dO"][rows]) < 1e-12
+            assert rel(grp["dxp"], bwd["dxp"][rows]) < 1e-12
+        else:
+            s = g - cfg.n_local
+            assert np.array_equal(rows, TK + s * cfg.T + np.arange(cfg.T))
+            assert rel(grp["O"], fwd["shared"][s][3]) < 1e-12
+            assert rel(grp["dxp"], bwd["shared"][s]["dh"]) < 1e-12
+        for wname in ("dW_gate", "dW_up", "dW_down"):
+            assert rel(grp[wname], bwd[wname][g]) < 1e-12, (g, wname)
+        seen.append(g)
+    # every group with rows is visited once, empty hosted experts are not
+    want = [g for g in range(cfg.n_local) if fwd["counts"][g]] + list(range(cfg.n_local, cfg.n_groups))
+    assert seen == want
+    tok = st["tokens"]
+    assert rel(tok["y"], fwd["y"]) < 1e-12
+    assert rel(tok["dgate"], bwd["dgate"]) < 1e-12
+    assert rel(tok["dx"], bwd["dx"]) < 1e-12
+    if cfg.router_backward:
+        assert rel(tok["dlogits"], bwd["dlogits"]) < 1e-12
+        assert rel(tok["dW_router"], bwd["dW_router"]) < 1e-12
+    else:
+        assert "dlogits" not in tok
 
 
 # ----------------------------------------------- planted mistakes: each pin catches its kind
