@@ -14,6 +14,7 @@ struct GemmArgs {
   const int32_t* mt_tail;     // [G+1] prefix of the groups' tail m-tiles (at most half their rows), or null
   const int32_t* order;       // [G] groups by decreasing row count (weight-gradient kinds), or null
   int n_tiles, m_tiles;       // tiles along N (all kinds) and along M (weight-gradient kinds)
+  int n_extent;               // output columns of the tile grid (FWD_GU: 2f); the last n-tile may hold fewer
   const void* x;              // [T, d]
   const void* xp;             // [T*k, d]
   const void* dy;             // [T, d]

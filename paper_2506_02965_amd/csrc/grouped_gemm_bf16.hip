@@ -310,6 +310,11 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
 
   const int q = lane >> 4, li = lane & 15;
   const bool wave_rows = !KT::ragged_m || m0 + wm * C::WTM < rows;  // wave-uniform
+  // The last n-tile of a contraction whose N is not a multiple of BN holds fewer columns (N is a multiple of
+  // 128 and a wave's columns a 64-aligned block, so each wave's columns are all inside or all past N). Its
+  // B loads past N read neighbouring rows or zeros through the buffer range check: finite values that reach
+  // only the columns past N, which are neither computed nor stored.
+  const bool wave_cols = n0 + wn * C::WTN < p.n_extent;  // wave-uniform
   for (int kt = 0; kt < KTN; ++kt) {
     // tile kt has landed when at most the later tiles' loads are outstanding
     if (kt + STAGES - 2 < KTN) wait_vmcnt<(STAGES - 2) * C::LOADS>();
@@ -317,8 +322,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
     // every wave's loads of tile kt have landed and its reads of the stage about to be refilled are done
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     if (kt + STAGES - 1 < KTN) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
-    // a wavefront whose rows all lie past the group's end has nothing to compute (it still loads and syncs)
-    if (!wave_rows) continue;
+    // a wavefront whose rows all lie past the group's end, or whose columns all lie past N, has nothing to
+    // compute (it still loads and syncs)
+    if (!wave_rows || !wave_cols) continue;
     const char* As = smem + (kt % STAGES) * C::STAGE_BYTES;
     const char* Bs = As + C::A_BYTES;
 #pragma unroll
@@ -367,6 +373,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
   __syncthreads();  // every wave is done with the operand buffers
 
   // ------------------------------------------------------------------ epilogue (per wave)
+  if (!wave_cols) return;  // no output column of this wave lies inside N (the epilogue has no workgroup barrier)
   float* st = reinterpret_cast<float*>(smem + wave * C::WAVE_EPI);
   constexpr int FPP = C::PART_ROWS / 16;  // fm blocks per part
   constexpr int OUT_W = (KIND == FWD_GU) ? C::WTN / 2 : C::WTN;  // output columns of the wave
@@ -642,11 +649,13 @@ static int device_cus() {
 }
 
 // Ragged-M contraction: n_cols output columns of the tile grid (FWD_GU: gate columns, two per pair).
-// A shape must tile M and N exactly (d_model, d_ff are multiples of 128): fall back to 128-wide sides.
+// A shape must tile M exactly (d_model, d_ff are multiples of 128), else it falls back to 128-wide sides. Along N
+// the 256 x 256 tile also takes a last n-tile of 128 columns (N an odd multiple of 128, e.g. d_ff = 1408): its
+// upper two wave columns skip their MFMAs and stores. Other shapes need N to be a multiple of their width.
 static int fit_shape(int sh, int M, int N) {
   int bm = kShapeBM[sh], bn = kShapeBN[sh];
   if (M > 0 && (M % bm || bm == 192)) bm = 128;  // weight gradients (K-major A) take no 192-row tiles
-  if (N % bn) bn = 128;
+  if (N % bn && !(sh == T256x256w16 && N % 128 == 0)) bn = 128;
   if (bm == kShapeBM[sh] && bn == kShapeBN[sh]) return sh;
   const bool k32 = sh == T256x256k32 || sh == T256x128k32 || sh == T128x128k32;
   if (sh == T256x256w16 || sh == T256x256w16k32s4 || sh == T256x256w16k32s3)
@@ -669,7 +678,8 @@ template <int KIND>
 static Prep prep_ragged(const moe_desc& d, GemmArgs a, const Plan& pl, int n_cols, bool tails_last = false) {
   const int sh = fit_shape(tile_shape(KIND, d), 0, n_cols);
   const int bm = kShapeBM[sh], bn = kShapeBN[sh];
-  a.n_tiles = n_cols / bn;  // FWD_GU: n_cols = 2f, each tile holds bn/2 gate and bn/2 up columns
+  a.n_tiles = (n_cols + bn - 1) / bn;  // FWD_GU: n_cols = 2f, each tile holds bn/2 gate and bn/2 up columns
+  a.n_extent = n_cols;
   const long bound = mtile_bound2(d, bm) * a.n_tiles;
   // 256-row tiles in more than one round of the chip, or sharing it with another contraction: tails after the
   // others (see decode_tile), so that every XCD gets an even share of both; its share of each segment is rounded
@@ -693,7 +703,8 @@ static Prep prep_wgrad(const moe_desc& d, GemmArgs a, const Plan& pl, int M, int
   }();
   a.wg_interleave = wgrr >= 0 ? (wgrr >> KIND) & 1 : (KIND == WG_GU ? 1 : 0);
   a.m_tiles = M / kShapeBM[sh];
-  a.n_tiles = N / kShapeBN[sh];
+  a.n_tiles = (N + kShapeBN[sh] - 1) / kShapeBN[sh];
+  a.n_extent = N;
   return Prep{sh, a, (long)(d.local_count + d.n_shared) * a.m_tiles * a.n_tiles};
 }
 template <int KIND>

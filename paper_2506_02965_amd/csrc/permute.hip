@@ -51,18 +51,38 @@ __global__ __launch_bounds__(256) void perm_scatter_kernel(const int32_t* __rest
   __shared__ int base[256];      // this block's first row per expert
   __shared__ int wsum[4];
   __shared__ int nloc_s;
+  __shared__ int part_before[256], part_tot[256];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   for (int i = threadIdx.x; i < 4 * lc; i += 256) wcnt[i] = 0;
   {
-    // expert e = thread: its total and the rows of the earlier blocks, then the exclusive prefix of the
-    // totals over experts (lc <= 256)
+    // Per expert, the rows of the earlier blocks and the total over all blocks. The nblk x lc count table is
+    // split over the block's threads: lcp (lc rounded up to a power of two, <= 256) experts by 256 / lcp parts
+    // of the blocks, each thread summing its part's column with its loads in flight together; the parts are
+    // then added in LDS, in part order.
+    const int lcp = lc <= 1 ? 1 : 1 << (32 - __builtin_clz(lc - 1));
+    const int nparts = 256 / lcp;
+    const int ep = threadIdx.x & (lcp - 1), part = threadIdx.x / lcp;
+    const int chunk = (nblk + nparts - 1) / nparts;
+    const int b0 = part * chunk, b1 = min(nblk, b0 + chunk);
+    int pb = 0, pt = 0;
+    if (ep < lc) {
+#pragma unroll 8
+      for (int b = b0; b < b1; ++b) {
+        const int c = blk_counts[(size_t)b * lc + ep];
+        pb += (b < (int)blockIdx.x) ? c : 0;
+        pt += c;
+      }
+    }
+    part_before[threadIdx.x] = pb;
+    part_tot[threadIdx.x] = pt;
+    __syncthreads();
+    // expert e = thread: then the exclusive prefix of the totals over experts (lc <= 256)
     const int e = threadIdx.x;
     int tot = 0, before = 0;
     if (e < lc)
-      for (int b = 0; b < nblk; ++b) {
-        const int c = blk_counts[(size_t)b * lc + e];
-        if (b < (int)blockIdx.x) before += c;
-        tot += c;
+      for (int q = 0; q < nparts; ++q) {
+        before += part_before[q * lcp + e];
+        tot += part_tot[q * lcp + e];
       }
     int incl = tot;
 #pragma unroll
