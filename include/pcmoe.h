@@ -119,6 +119,19 @@ moe_status moe_permute(const moe_desc* desc, const int32_t* topk_idx, const void
                        void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * moe_permute without a workspace argument, for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc). Same arguments, outputs and errors as
+ * moe_permute, bit for bit the same results. Its scratch is a fixed 1 MiB device array inside the library, one
+ * per GPU, held until the process ends (looked up on the first call on each device); the call allocates
+ * nothing. MOE_ERR_UNSUPPORTED when the shape needs more scratch than that:
+ * ceil(T*k / 1024) * local_count * 4 bytes > 1 MiB. Every call on one GPU shares that scratch: calls that overlap
+ * in time on the same GPU (concurrent streams, or threads) race and must be serialised by the caller.
+ */
+moe_status moe_permute_noalloc(const moe_desc* desc, const int32_t* topk_idx, const void* x, int32_t* counts,
+                               int32_t* offsets, int32_t* row_to_slot, int32_t* slot_to_row, void* x_perm,
+                               hipStream_t stream);
+
+/*
  * ForwardExpert of Alg. 6 for every hosted expert and every shared expert (grouped GEMMs):
  * G = h W_gate^T, U = h W_up^T, H = silu(G) * U, O = H W_down^T.
  *   x       [T, d]  dtype: input rows of the shared experts

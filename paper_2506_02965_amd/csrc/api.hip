@@ -196,6 +196,22 @@ moe_status moe_permute(const moe_desc* d, const int32_t* topk_idx, const void* x
                     "moe_permute");
 }
 
+moe_status moe_permute_noalloc(const moe_desc* d, const int32_t* topk_idx, const void* x, int32_t* counts,
+                               int32_t* offsets, int32_t* row_to_slot, int32_t* slot_to_row, void* x_perm,
+                               hipStream_t stream) {
+  moe_status st = check_desc(d);
+  if (st) return st;
+  NEED(topk_idx); NEED(x); NEED(counts); NEED(offsets); NEED(row_to_slot); NEED(slot_to_row); NEED(x_perm);
+  const size_t need = permute_ws_bytes(*d);
+  if (need > permute_noalloc_capacity())
+    return fail(MOE_ERR_UNSUPPORTED, "moe_permute_noalloc: %zu bytes of scratch needed, its fixed scratch holds %zu",
+                need, permute_noalloc_capacity());
+  void* ws = nullptr;
+  if (hipError_t e = permute_noalloc_scratch(&ws); e != hipSuccess) return hip_status(e, "moe_permute_noalloc");
+  return hip_status(launch_permute(*d, topk_idx, x, counts, offsets, row_to_slot, slot_to_row, x_perm, ws, stream),
+                    "moe_permute_noalloc");
+}
+
 moe_status moe_expert_ffn_fwd(const moe_desc* d, const void* x, const void* x_perm, const int32_t* offsets,
                               const void* w_gate, const void* w_up, const void* w_down, void* y_perm, void* saved,
                               void* ws, size_t ws_bytes, hipStream_t stream) {

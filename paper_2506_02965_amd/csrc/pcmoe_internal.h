@@ -140,6 +140,8 @@ size_t route_bwd_ws_bytes(const moe_desc& d);
 hipError_t launch_permute(const moe_desc& d, const int32_t* idx, const void* x, int32_t* counts, int32_t* offsets,
                           int32_t* r2s, int32_t* s2r, void* xp, void* ws, hipStream_t s);
 size_t permute_ws_bytes(const moe_desc& d);
+size_t permute_noalloc_capacity();                // bytes of the fixed scratch of moe_permute_noalloc
+hipError_t permute_noalloc_scratch(void** out);   // its device address on the current device
 hipError_t launch_permute_bwd(const moe_desc& d, const void* dxp, const int32_t* s2r, const float* dlogits,
                               const void* wr, void* dx, hipStream_t s);
 

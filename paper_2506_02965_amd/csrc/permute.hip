@@ -195,6 +195,32 @@ size_t permute_ws_bytes(const moe_desc& d) {
   return align256(nblk * d.local_count * sizeof(int32_t));
 }
 
+// ------------------------------------------------------------------ allocation-free dispatch
+// The scratch of moe_permute_noalloc: the per-block expert counts (ceil(T*k / PM_SLOTS) x local_count int32) in a
+// device array of fixed size. Each GPU the library runs on holds its own copy until the process ends; every call
+// on that GPU shares it. Nothing in it needs clearing: the histogram launch writes every count the scatter reads.
+constexpr size_t kNoallocScratchBytes = size_t(1) << 20;
+static __device__ __align__(256) char scratch[kNoallocScratchBytes];
+
+size_t permute_noalloc_capacity() { return kNoallocScratchBytes; }
+
+// Device address of `scratch` on the current device, looked up once per device with that device current.
+// The array's host-side name is no device address: kernels and copies take the pointer returned here.
+hipError_t permute_noalloc_scratch(void** out) {
+  static std::atomic<void*> addr[64];
+  int dev = 0;
+  if (hipError_t e = hipGetDevice(&dev); e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  void* p = addr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    if (hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)); e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev].store(p, std::memory_order_release);  // concurrent first calls store the same address
+  }
+  *out = p;
+  return hipSuccess;
+}
+
 static int gather_blocks(int Tn) {
   int b = (Tn + 3) / 4;
   return b > 8192 ? 8192 : (b < 1 ? 1 : b);

@@ -18,7 +18,7 @@ MOE_F32, MOE_BF16 = 0, 1
 MOE_WS_PERMUTE, MOE_WS_FFN_SAVED, MOE_WS_FFN_FWD, MOE_WS_FFN_BWD, MOE_WS_ROUTE_BWD = range(5)
 
 # every symbol include/pcmoe.h declares
-EXPORTS = ("moe_workspace_size", "moe_route", "moe_permute", "moe_expert_ffn_fwd", "moe_combine", "moe_combine_bwd",
+EXPORTS = ("moe_workspace_size", "moe_route", "moe_permute", "moe_permute_noalloc", "moe_expert_ffn_fwd", "moe_combine", "moe_combine_bwd",
            "moe_expert_ffn_bwd", "moe_route_bwd", "moe_permute_bwd", "moe_expert_update", "moe_kernel_timing",
            "moe_kernel_timing_select", "moe_kernel_timing_report", "moe_status_string", "moe_last_error")
 MOE_OPT_SGD, MOE_OPT_ADAMW = 0, 1
@@ -63,6 +63,7 @@ def lib():
             "moe_workspace_size": (_SZ, [D, _INT]),
             "moe_route": (_INT, [D, _VP, _VP, _VP, _I32, _VP, _VP, _VP, _VP]),
             "moe_permute": (_INT, [D, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
+            "moe_permute_noalloc": (_INT, [D, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
             "moe_expert_ffn_fwd": (_INT, [D, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
             "moe_combine": (_INT, [D, _VP, _VP, _VP, _VP, _VP]),
             "moe_combine_bwd": (_INT, [D, _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
@@ -137,6 +138,12 @@ def moe_permute(desc, topk_idx, x, counts, offsets, row_to_slot, slot_to_row, x_
     _check("moe_permute", lib().moe_permute(ctypes.byref(desc), _ptr(topk_idx), _ptr(x), _ptr(counts), _ptr(offsets),
                                             _ptr(row_to_slot), _ptr(slot_to_row), _ptr(x_perm), _ptr(ws), ws_bytes,
                                             _stream(stream)))
+
+
+def moe_permute_noalloc(desc, topk_idx, x, counts, offsets, row_to_slot, slot_to_row, x_perm, stream=None):
+    _check("moe_permute_noalloc", lib().moe_permute_noalloc(
+        ctypes.byref(desc), _ptr(topk_idx), _ptr(x), _ptr(counts), _ptr(offsets), _ptr(row_to_slot),
+        _ptr(slot_to_row), _ptr(x_perm), _stream(stream)))
 
 
 def moe_expert_ffn_fwd(desc, x, x_perm, offsets, w_gate, w_up, w_down, y_perm, saved, ws, ws_bytes, stream=None):

@@ -22,7 +22,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 15, names
+    assert len(names) == 16, names
     assert sorted(P.EXPORTS) == names
     L = P.lib()
     for n in names:
@@ -90,6 +90,18 @@ def test_extent_limits_admit_the_workloads():
     assert P.moe_workspace_size(ok, P.MOE_WS_FFN_SAVED) > 0
     over = desc(T=t_max + 1, d_model=4096, d_ff=14336, n_experts=8, top_k=2, dtype="bf16")
     assert P.moe_workspace_size(over, P.MOE_WS_FFN_SAVED) == 0
+
+
+def test_permute_noalloc_refuses_beyond_its_scratch():
+    """The allocation-free dispatch has a fixed 1 MiB scratch: ceil(T*k / 1024) * local_count * 4 bytes must fit."""
+    ok = desc(T=262144, d_model=128, d_ff=128, n_experts=256, top_k=4)        # 1024 blocks x 256 experts: 1 MiB
+    with pytest.raises(P.MoeError) as ei:
+        P.moe_permute_noalloc(ok, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, stream=0)   # refused for x_perm only
+    assert ei.value.status == P.MOE_ERR_INVALID_ARGUMENT and "x_perm" in P.last_error()
+    big = desc(T=262144 + 256, d_model=128, d_ff=128, n_experts=256, top_k=4)  # 1025 blocks
+    with pytest.raises(P.MoeError) as ei:
+        P.moe_permute_noalloc(big, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, stream=0)
+    assert ei.value.status == P.MOE_ERR_UNSUPPORTED and "scratch" in P.last_error()
 
 
 def test_null_pointers_and_workspace():
