@@ -11,13 +11,15 @@ static int token_blocks(int Tn) {
   return b > 8192 ? 8192 : (b < 1 ? 1 : b);
 }
 
-// Each lane handles CPL 16-byte chunks per pass; the chunks of all KM slots are loaded together (one round
-// trip per token for its map and weights, one for its rows).
-template <typename T, int KM, int CPL>
+// Each lane handles CPL 16-byte chunks per pass; the chunks of all KM slots and of up to SM shared experts are
+// loaded together (one round trip per token for its map and weights, one per pass for its rows); shared
+// experts beyond SM are added one at a time after them. Sums: slots j in order, then shared experts in order.
+template <typename T, int KM, int SM>
 __global__ __launch_bounds__(256) void combine_kernel(int Tn, int k, int S, int cpr, const Chunk* __restrict__ yp,
                                                       const int32_t* __restrict__ s2r,
                                                       const float* __restrict__ gw, Chunk* __restrict__ y) {
   constexpr int N = EPC<T>::value;
+  constexpr int CPL = chunks_per_lane(KM + SM);
   const int lane = threadIdx.x & 63;
   const int wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int nwaves = (gridDim.x * blockDim.x) >> 6;
@@ -31,12 +33,17 @@ __global__ __launch_bounds__(256) void combine_kernel(int Tn, int k, int S, int 
       w[j] = (j < k) ? gw[(size_t)t * k + j] : 0.f;
     }
     for (int c0 = lane; c0 < cpr; c0 += 64 * CPL) {
-      Chunk in[KM][CPL];
+      Chunk in[KM][CPL], sh[SM > 0 ? SM : 1][CPL];
 #pragma unroll
       for (int j = 0; j < KM; ++j)
 #pragma unroll
         for (int u = 0; u < CPL; ++u)
           in[j][u] = (rows[j] >= 0 && c0 + 64 * u < cpr) ? yp[(size_t)rows[j] * cpr + c0 + 64 * u] : zero_chunk();
+#pragma unroll
+      for (int s = 0; s < SM; ++s)
+#pragma unroll
+        for (int u = 0; u < CPL; ++u)
+          sh[s][u] = (c0 + 64 * u < cpr) ? yp[(shared_base + (size_t)s * Tn + t) * cpr + c0 + 64 * u] : zero_chunk();
 #pragma unroll
       for (int u = 0; u < CPL; ++u) {
         const int c = c0 + 64 * u;
@@ -51,9 +58,15 @@ __global__ __launch_bounds__(256) void combine_kernel(int Tn, int k, int S, int 
             for (int i = 0; i < N; ++i) acc[i] = fmaf(w[j], v[i], acc[i]);
           }
         }
+#pragma unroll
+        for (int s = 0; s < SM; ++s) {
+          chunk_to_f<T>(sh[s][u], v);
+#pragma unroll
+          for (int i = 0; i < N; ++i) acc[i] += v[i];
+        }
         if (c < cpr) {
-          for (int sh = 0; sh < S; ++sh) {
-            chunk_to_f<T>(yp[(shared_base + (size_t)sh * Tn + t) * cpr + c], v);
+          for (int s = SM; s < S; ++s) {
+            chunk_to_f<T>(yp[(shared_base + (size_t)s * Tn + t) * cpr + c], v);
 #pragma unroll
             for (int i = 0; i < N; ++i) acc[i] += v[i];
           }
@@ -125,13 +138,13 @@ hipError_t launch_combine(const moe_desc& d, const void* yp, const int32_t* s2r,
                           hipStream_t s) {
   const int cpr = (int)(d.d_model * elem_bytes(d) / 16);
   KernelTimer kt("combine", s);
-  row_dispatch(d.top_k, cpr, [&](auto km, auto cpl) {
-    constexpr int KM = decltype(km)::value, CPL = decltype(cpl)::value;
+  batch_dispatch(d.top_k, d.n_shared, false, [&](auto km, auto sm, auto) {
+    constexpr int KM = decltype(km)::value, SM = decltype(sm)::value;
     if (d.dtype == MOE_BF16)
-      hipLaunchKernelGGL((combine_kernel<bf16, KM, CPL>), dim3(token_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k,
+      hipLaunchKernelGGL((combine_kernel<bf16, KM, SM>), dim3(token_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k,
                          d.n_shared, cpr, (const Chunk*)yp, s2r, w, (Chunk*)y);
     else
-      hipLaunchKernelGGL((combine_kernel<float, KM, CPL>), dim3(token_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k,
+      hipLaunchKernelGGL((combine_kernel<float, KM, SM>), dim3(token_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k,
                          d.n_shared, cpr, (const Chunk*)yp, s2r, w, (Chunk*)y);
   });
   return hipGetLastError();

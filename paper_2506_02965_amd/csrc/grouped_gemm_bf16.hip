@@ -214,32 +214,27 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
     b_ld = d * ES;
   }
 
-  // K-major operands in the padded layout (mk_row)
-  constexpr bool MKP_A = !KT::a_kc && BM == 256 && C::WTM == 64;
-  constexpr bool MKP_B = !KT::b_kc && BN == 256 && C::WTN == 64;
+  // K-major operands in the padded layout (mk_row); a 128-wide wave tile reads two of its 64-column blocks
+  constexpr bool MKP_A = !KT::a_kc && BM == 256 && (C::WTM == 64 || C::WTM == 128);
+  constexpr bool MKP_B = !KT::b_kc && BN == 256 && (C::WTN == 64 || C::WTN == 128);
 
-  // per-lane byte offsets of each direct-load instruction at K-tile 0
-  int va[C::IA], vb[C::IB];
-  bool bup[C::IB];  // FWD_GU: instruction reads W_up rows
-#pragma unroll
-  for (int j = 0; j < C::IA; ++j) {
-    const int jj = wave + C::NW * j;
+  // Per-lane byte offset at K-tile 0 of direct-load instruction jj (0 .. BM*ROWB/1024 - 1) of each operand;
+  // for FWD_GU also whether the instruction's rows are W_up rows.
+  const auto a_off = [&](int jj) {
     if (KT::a_kc) {
       const int r = C::RPI * jj + lane / C::CR, c = (lane % C::CR) ^ kc_swz<BK>(r);
-      va[j] = (m0 + r) * a_ld + 16 * c;
+      return (m0 + r) * a_ld + 16 * c;
     } else if (MKP_A) {
       const int kr = 2 * jj + (lane >> 5), c = ((lane & 31) - 8 * (kr & 1)) & 31;
-      va[j] = kr * a_ld + (m0 + 8 * c) * ES;
+      return kr * a_ld + (m0 + 8 * c) * ES;
     } else {
       constexpr int CPR = BM / 8;
       const int slot = 64 * jj + lane, kr = slot / CPR, c = (slot % CPR) ^ mc_swz(kr);
-      va[j] = kr * a_ld + (m0 + 8 * c) * ES;
+      return kr * a_ld + (m0 + 8 * c) * ES;
     }
-  }
-#pragma unroll
-  for (int j = 0; j < C::IB; ++j) {
-    const int jj = wave + C::NW * j;
-    bup[j] = false;
+  };
+  const auto b_off = [&](int jj, bool& up) {
+    up = false;
     if (KT::b_kc) {
       const int r = C::RPI * jj + lane / C::CR, c = (lane % C::CR) ^ kc_swz<BK>(r);
       int wrow;
@@ -247,53 +242,42 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
         const int wcol = r / C::WTN, within = r % C::WTN, half = C::WTN / 2;
         static_assert((C::WTN / 2) % C::RPI == 0, "a direct load must not straddle gate and up rows");
         wrow = ti.nt * (BN / 2) + wcol * half + (within % half);
-        bup[j] = ((C::RPI * jj) % C::WTN) >= half;  // the instruction's rows are all gate or all up rows
+        up = ((C::RPI * jj) % C::WTN) >= half;  // the instruction's rows are all gate or all up rows
       } else {
         wrow = n0 + r;
       }
-      vb[j] = wrow * b_ld + 16 * c;
+      return wrow * b_ld + 16 * c;
     } else if (MKP_B) {
       const int kr = 2 * jj + (lane >> 5), c = ((lane & 31) - 8 * (kr & 1)) & 31;
-      vb[j] = kr * b_ld + (n0 + 8 * c) * ES;
+      return kr * b_ld + (n0 + 8 * c) * ES;
     } else {
       constexpr int CPR = BN / 8;
       const int slot = 64 * jj + lane, kr = slot / CPR, c = (slot % CPR) ^ mc_swz(kr);
-      vb[j] = kr * b_ld + (n0 + 8 * c) * ES;
-    }
-  }
-
-  // Direct load number idx (0 .. LOADS-1) of K-tile kt into LDS stage `stage`.
-  const uint32_t lds0 = lds_addr(smem) + wave * 1024;
-  auto issue_one = [&](int kt, int stage, int idx) {
-    const uint32_t As = lds0 + stage * C::STAGE_BYTES;
-    const uint32_t Bs = As + C::A_BYTES;
-    const int k0 = kt * BK;
-    // padding before instruction jj = wave + NW * j: K-contiguous rows RPI * jj .. RPI * jj + RPI - 1
-    // follow 16 bytes per earlier 16 rows; a padded K-major block follows 32 bytes per earlier block
-    const auto pad = [&](int j, bool kc, bool mkp) {
-      const int jj = wave + C::NW * j;
-      return kc ? 16 * ((C::RPI * jj) >> 4) : (mkp ? 32 * jj : 0);
-    };
-    if (idx < C::IA) {
-      const int j = idx;
-      // Row-ragged tiles: an instruction whose rows all lie past the group's end is skipped (two-stage ring,
-      // where the waits are vmcnt(0)); those rows' outputs are never stored, and no other row reads them.
-      if (KT::ragged_m && STAGES == 2 && m0 + C::RPI * (wave + C::NW * j) >= rows) return;
-      dma16(ra, As + C::NW * j * 1024 + pad(j, KT::a_kc, MKP_A), va[j] + (KT::a_kc ? k0 * ES : k0 * a_ld));
-    } else {
-      const int j = idx - C::IA;
-      if (KIND == BWD_DX) {
-        const bool up = k0 >= f;
-        dma16(up ? rb1 : rb0, Bs + C::NW * j * 1024 + pad(j, false, MKP_B), vb[j] + (up ? k0 - f : k0) * b_ld);
-      } else {
-        dma16(bup[j] ? rb1 : rb0, Bs + C::NW * j * 1024 + pad(j, KT::b_kc, MKP_B),
-              vb[j] + (KT::b_kc ? k0 * ES : k0 * b_ld));
-      }
+      return kr * b_ld + (n0 + 8 * c) * ES;
     }
   };
-  auto issue = [&](int kt, int stage) {
-#pragma unroll
-    for (int idx = 0; idx < C::LOADS; ++idx) issue_one(kt, stage, idx);
+  // LDS padding before instruction jj: K-contiguous rows RPI * jj .. RPI * jj + RPI - 1 follow 16 bytes per
+  // earlier 16 rows; a padded K-major block follows 32 bytes per earlier block
+  const auto pad = [&](int jj, bool kc, bool mkp) { return kc ? 16 * ((C::RPI * jj) >> 4) : (mkp ? 32 * jj : 0); };
+  const uint32_t lds_base = lds_addr(smem);
+  // Direct load of instruction jj of operand A (or B) of K-tile kt into LDS stage `stage`.
+  const auto load_a = [&](int kt, int stage, int jj, int voff) {
+    // Row-ragged tiles in a two-stage ring (whose waits are vmcnt(0)): an instruction whose rows all lie past the
+    // group's end is skipped; those rows' outputs are never stored, and no other row reads them.
+    if (KT::ragged_m && STAGES == 2 && m0 + C::RPI * jj >= rows) return;
+    const int k0 = kt * BK;
+    dma16(ra, lds_base + stage * C::STAGE_BYTES + jj * 1024 + pad(jj, KT::a_kc, MKP_A),
+          voff + (KT::a_kc ? k0 * ES : k0 * a_ld));
+  };
+  const auto load_b = [&](int kt, int stage, int jj, int voff, bool up) {
+    const int k0 = kt * BK;
+    const uint32_t dst = lds_base + stage * C::STAGE_BYTES + C::A_BYTES + jj * 1024 + pad(jj, KT::b_kc, MKP_B);
+    if (KIND == BWD_DX) {
+      const bool hi = k0 >= f;  // K rows >= f are W_up rows
+      dma16(hi ? rb1 : rb0, dst, voff + (hi ? k0 - f : k0) * b_ld);
+    } else {
+      dma16(up ? rb1 : rb0, dst, voff + (KT::b_kc ? k0 * ES : k0 * b_ld));
+    }
   };
 
   floatx4 acc[C::FM][C::FN];
@@ -303,11 +287,6 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
     for (int j = 0; j < C::FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   const int KTN = (K + BK - 1) / BK;
-  // prologue: STAGES-1 tiles in flight
-#pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s)
-    if (s < KTN) issue(s, s);
-
   const int q = lane >> 4, li = lane & 15;
   const bool wave_rows = !KT::ragged_m || m0 + wm * C::WTM < rows;  // wave-uniform
   // The last n-tile of a contraction whose N is not a multiple of BN holds fewer columns (N is a multiple of
@@ -315,6 +294,66 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
   // B loads past N read neighbouring rows or zeros through the buffer range check: finite values that reach
   // only the columns past N, which are neither computed nor stored.
   const bool wave_cols = n0 + wn * C::WTN < p.n_extent;  // wave-uniform
+
+  // The operand fragments of MFMA k-step kk (32 deep) of the K-tile in stage `st`.
+  const auto read_frags = [&](const char* As, const char* Bs, int kk, Chunk (&a)[C::FM], Chunk (&b)[C::FN]) {
+    // K-contiguous fragments: row 16 * i + li of the wave's rows; the swizzle sees only li, and
+    // fragment i sits FRAG bytes after fragment 0 (an immediate offset of the LDS read)
+    constexpr int FRAG = 16 * C::ROWB + 16;
+    const int lane_kc = li * C::ROWB + (((4 * kk + q) ^ kc_swz<BK>(li)) << 4);
+    // padded K-major fragments: the lane's two k-rows (kl1, kl2) and its 8-byte column group; fragment i of a
+    // wave tile lies in 64-column block (wave offset + 16 i) / 64, at 32 (i mod 4) bytes
+    const int kl1 = 8 * q + 4 * (q & 1) + (li >> 2), kl2 = kl1 + 4 - 8 * (q & 1);
+    const int lane_mk = 16 * ((li & 3) >> 1) + 8 * (li & 1) + 16 * MK_BLOCK * kk;
+    const auto mk_lane = [&](int kl, int w) { return mk_row(kl) + 128 * ((w + (kl & 1)) & 3) + lane_mk; };
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i) {
+      if (KT::a_kc) {
+        a[i] = lds_kc_pair(As + kc_row<C::ROWB>(wm * C::WTM) + lane_kc + i * FRAG, q);
+      } else if (MKP_A) {
+        const int w = (wm * C::WTM) / 64 + i / 4;
+        a[i] = lds_tr_pair(As + mk_lane(kl1, w) + 32 * (i % 4), As + mk_lane(kl2, w) + 32 * (i % 4));
+      } else {
+        const int k1 = 32 * kk + 8 * q + 4 * (q & 1) + (li >> 2), mn = wm * C::WTM + 16 * i + 4 * (li & 3);
+        const int k2 = k1 + 4 - 8 * (q & 1);
+        a[i] = lds_tr_pair(As + k1 * (BM * 2) + (((mn >> 3) ^ mc_swz(k1)) << 4) + (mn & 7) * 2,
+                           As + k2 * (BM * 2) + (((mn >> 3) ^ mc_swz(k2)) << 4) + (mn & 7) * 2);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) {
+      if (KT::b_kc) {
+        b[j] = lds_kc_pair(Bs + kc_row<C::ROWB>(wn * C::WTN) + lane_kc + j * FRAG, q);
+      } else if (MKP_B) {
+        const int w = (wn * C::WTN) / 64 + j / 4;
+        b[j] = lds_tr_pair(Bs + mk_lane(kl1, w) + 32 * (j % 4), Bs + mk_lane(kl2, w) + 32 * (j % 4));
+      } else {
+        const int k1 = 32 * kk + 8 * q + 4 * (q & 1) + (li >> 2), mn = wn * C::WTN + 16 * j + 4 * (li & 3);
+        const int k2 = k1 + 4 - 8 * (q & 1);
+        b[j] = lds_tr_pair(Bs + k1 * (BN * 2) + (((mn >> 3) ^ mc_swz(k1)) << 4) + (mn & 7) * 2,
+                           Bs + k2 * (BN * 2) + (((mn >> 3) ^ mc_swz(k2)) << 4) + (mn & 7) * 2);
+      }
+    }
+  };
+
+  // Every wave loads IA + IB instructions of each K-tile (instruction jj = wave + NW j) and reads its fragments
+  // one 32-deep k-step at a time; loads run one K-tile ahead of the MFMAs.
+  int va[C::IA], vb[C::IB];
+  bool bup[C::IB];
+#pragma unroll
+  for (int j = 0; j < C::IA; ++j) va[j] = a_off(wave + C::NW * j);
+#pragma unroll
+  for (int j = 0; j < C::IB; ++j) vb[j] = b_off(wave + C::NW * j, bup[j]);
+  auto issue = [&](int kt, int stage) {
+#pragma unroll
+    for (int j = 0; j < C::IA; ++j) load_a(kt, stage, wave + C::NW * j, va[j]);
+#pragma unroll
+    for (int j = 0; j < C::IB; ++j) load_b(kt, stage, wave + C::NW * j, vb[j], bup[j]);
+  };
+  // prologue: STAGES-1 tiles in flight
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < KTN) issue(s, s);
   for (int kt = 0; kt < KTN; ++kt) {
     // tile kt has landed when at most the later tiles' loads are outstanding
     if (kt + STAGES - 2 < KTN) wait_vmcnt<(STAGES - 2) * C::LOADS>();
@@ -330,40 +369,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
 #pragma unroll
     for (int kk = 0; kk < C::KK; ++kk) {
       Chunk a[C::FM], b[C::FN];
-      // K-contiguous fragments: row 16 * i + li of the wave's rows; the swizzle sees only li, and
-      // fragment i sits FRAG bytes after fragment 0 (an immediate offset of the LDS read)
-      constexpr int FRAG = 16 * C::ROWB + 16;
-      const int lane_kc = li * C::ROWB + (((4 * kk + q) ^ kc_swz<BK>(li)) << 4);
-      // padded K-major fragments: the lane's two k-rows (kl1, kl2) and its 8-byte column group
-      const int kl1 = 8 * q + 4 * (q & 1) + (li >> 2), kl2 = kl1 + 4 - 8 * (q & 1);
-      const int lane_mk = 16 * ((li & 3) >> 1) + 8 * (li & 1) + 16 * MK_BLOCK * kk;
-      const auto mk_lane = [&](int kl, int w) { return mk_row(kl) + 128 * ((w + (kl & 1)) & 3) + lane_mk; };
-#pragma unroll
-      for (int i = 0; i < C::FM; ++i) {
-        if (KT::a_kc) {
-          a[i] = lds_kc_pair(As + kc_row<C::ROWB>(wm * C::WTM) + lane_kc + i * FRAG, q);
-        } else if (MKP_A) {
-          a[i] = lds_tr_pair(As + mk_lane(kl1, wm) + 32 * i, As + mk_lane(kl2, wm) + 32 * i);
-        } else {
-          const int k1 = 32 * kk + 8 * q + 4 * (q & 1) + (li >> 2), mn = wm * C::WTM + 16 * i + 4 * (li & 3);
-          const int k2 = k1 + 4 - 8 * (q & 1);
-          a[i] = lds_tr_pair(As + k1 * (BM * 2) + (((mn >> 3) ^ mc_swz(k1)) << 4) + (mn & 7) * 2,
-                             As + k2 * (BM * 2) + (((mn >> 3) ^ mc_swz(k2)) << 4) + (mn & 7) * 2);
-        }
-      }
-#pragma unroll
-      for (int j = 0; j < C::FN; ++j) {
-        if (KT::b_kc) {
-          b[j] = lds_kc_pair(Bs + kc_row<C::ROWB>(wn * C::WTN) + lane_kc + j * FRAG, q);
-        } else if (MKP_B) {
-          b[j] = lds_tr_pair(Bs + mk_lane(kl1, wn) + 32 * j, Bs + mk_lane(kl2, wn) + 32 * j);
-        } else {
-          const int k1 = 32 * kk + 8 * q + 4 * (q & 1) + (li >> 2), mn = wn * C::WTN + 16 * j + 4 * (li & 3);
-          const int k2 = k1 + 4 - 8 * (q & 1);
-          b[j] = lds_tr_pair(Bs + k1 * (BN * 2) + (((mn >> 3) ^ mc_swz(k1)) << 4) + (mn & 7) * 2,
-                             Bs + k2 * (BN * 2) + (((mn >> 3) ^ mc_swz(k2)) << 4) + (mn & 7) * 2);
-        }
-      }
+      read_frags(As, Bs, kk, a, b);
 #pragma unroll
       for (int i = 0; i < C::FM; ++i)
 #pragma unroll

@@ -107,6 +107,30 @@ inline void row_dispatch(int k, int cpr, F&& f) {
   else with_km(std::integral_constant<int, 8>{});
 }
 
+// Per-token row kernels that load several rows of a token at once: KM = top_k rounded up to 1, 2, 4, 6 or 8,
+// SM = min(n_shared, 2) shared-expert rows loaded with them, and whether a router term is added (DL). f receives
+// the three as std::integral_constant / std::bool_constant.
+template <typename F>
+inline void batch_dispatch(int k, int S, bool dl, F&& f) {
+  auto with_sm = [&](auto km) {
+    auto with_dl = [&](auto sm) {
+      if (dl) f(km, sm, std::bool_constant<true>{});
+      else f(km, sm, std::bool_constant<false>{});
+    };
+    if (S <= 0) with_dl(std::integral_constant<int, 0>{});
+    else if (S == 1) with_dl(std::integral_constant<int, 1>{});
+    else with_dl(std::integral_constant<int, 2>{});
+  };
+  if (k <= 1) with_sm(std::integral_constant<int, 1>{});
+  else if (k <= 2) with_sm(std::integral_constant<int, 2>{});
+  else if (k <= 4) with_sm(std::integral_constant<int, 4>{});
+  else if (k <= 6) with_sm(std::integral_constant<int, 6>{});
+  else with_sm(std::integral_constant<int, 8>{});
+}
+// 16-byte chunks per lane per pass for a kernel that keeps `rows` rows' chunks in flight at once (at most 32
+// chunks, 128 VGPRs, of loads per lane).
+constexpr int chunks_per_lane(int rows) { return rows <= 8 ? 4 : (rows <= 16 ? 2 : 1); }
+
 // Bracket a kernel launch with HIP events when per-kernel timing is on (no-op otherwise).
 struct KernelTimer {
   KernelTimer(const char* name, hipStream_t s);

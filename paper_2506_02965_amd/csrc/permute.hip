@@ -3,6 +3,7 @@
 // and the hand-back of the input gradient (Sec. 3.2), summed per token.
 //
 // Ordering is reproducible bit for bit: rows of one expert are in increasing slot order.
+//   0. up to PS_MAX slots: histogram, scan and scatter in one workgroup (perm_sort_small_kernel); beyond:
 //   1. histogram: per block of PM_SLOTS slots, per hosted expert counts (LDS atomics; order-free)
 //   2. scatter: each block first derives its own base per expert from the histogram (the exclusive
 //      prefix over experts of the totals, plus the counts of the earlier blocks; block 0 also writes
@@ -153,6 +154,107 @@ __global__ __launch_bounds__(256) void perm_scatter_kernel(const int32_t* __rest
   }
 }
 
+// Up to PS_MAX slots: the histogram, the scan and the stable scatter in one workgroup of 16 wavefronts, no
+// count table between launches. Wavefront w ranks slots [w * per_wave, (w + 1) * per_wave) in order, 64 at a
+// time, with the same peer-mask ballots as the scatter above; its per-expert bases follow the earlier wavefronts'
+// counts, so rows of one expert stay in increasing slot order.
+constexpr int PS_WAVES = 16, PS_ITERS = 16, PS_MAX = PS_WAVES * PS_ITERS * 64;
+
+__global__ __launch_bounds__(1024) void perm_sort_small_kernel(const int32_t* __restrict__ idx, int nslots, int lb,
+                                                               int lc, int nbits, int32_t* __restrict__ counts,
+                                                               int32_t* __restrict__ offsets,
+                                                               int32_t* __restrict__ r2s, int32_t* __restrict__ s2r) {
+  extern __shared__ int wcnt[];  // [PS_WAVES][lc]: per-wave counts, then per-wave first rows
+  __shared__ int tot_s[256], base_s[256];
+  __shared__ int nloc_s;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int per_wave = (nslots + PS_WAVES * 64 - 1) / (PS_WAVES * 64) * 64;  // a multiple of 64, <= 1024
+  const int a_w = w * per_wave;
+  for (int i = threadIdx.x; i < PS_WAVES * lc; i += 1024) wcnt[i] = 0;
+  int v_of[PS_ITERS];  // local expert of each of the lane's slots, -1 if hosted elsewhere or past the end
+#pragma unroll
+  for (int it = 0; it < PS_ITERS; ++it) {
+    const int a = a_w + it * 64 + lane;
+    int v = -1;
+    if (it * 64 < per_wave && a < nslots) {
+      v = idx[a] - lb;
+      if (v < 0 || v >= lc) v = -1;
+    }
+    v_of[it] = v;
+  }
+  __syncthreads();
+  const uint64_t lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
+  int* mine = wcnt + w * lc;
+  // pass 1: per-wave counts (the lowest lane of each peer group adds the group's size)
+#pragma unroll
+  for (int it = 0; it < PS_ITERS; ++it) {
+    if (it * 64 >= per_wave) break;  // wave-uniform
+    const int v = v_of[it];
+    const uint64_t peers = peer_mask(v < 0 ? 0 : v, v >= 0, nbits);
+    if (v >= 0 && (peers & lt) == 0) mine[v] += __popcll(peers);
+  }
+  __syncthreads();
+  // per expert: each wave's first row within the expert, and the expert's total
+  for (int e = threadIdx.x; e < lc; e += 1024) {
+    int r = 0;
+    for (int ww = 0; ww < PS_WAVES; ++ww) {
+      const int c = wcnt[ww * lc + e];
+      wcnt[ww * lc + e] = r;
+      r += c;
+    }
+    tot_s[e] = r;
+  }
+  __syncthreads();
+  // exclusive prefix of the totals over experts (lc <= 256), by the first wavefront
+  if (w == 0) {
+    int carry = 0;
+    for (int q = 0; q < 4; ++q) {
+      const int e = 64 * q + lane;
+      const int t = (e < lc) ? tot_s[e] : 0;
+      int incl = t;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const int o = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += o;
+      }
+      if (e < lc) {
+        base_s[e] = carry + incl - t;
+        counts[e] = t;
+        offsets[e] = carry + incl - t;
+      }
+      carry += __shfl(incl, 63, 64);
+    }
+    if (lane == 0) {
+      offsets[lc] = carry;
+      nloc_s = carry;
+    }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < PS_WAVES * lc; i += 1024) wcnt[i] += base_s[i % lc];
+  __syncthreads();
+  // pass 2: stable ranks
+#pragma unroll
+  for (int it = 0; it < PS_ITERS; ++it) {
+    if (it * 64 >= per_wave) break;
+    const int a = a_w + it * 64 + lane;
+    const int v = v_of[it];
+    const uint64_t peers = peer_mask(v < 0 ? 0 : v, v >= 0, nbits);
+    if (a < nslots) {
+      if (v >= 0) {
+        const int pos = mine[v] + __popcll(peers & lt);
+        r2s[pos] = a;
+        s2r[a] = pos;
+      } else {
+        s2r[a] = -1;
+      }
+    }
+    if (v >= 0 && (peers & lt) == 0) mine[v] += __popcll(peers);
+  }
+  // rows beyond N_loc have no slot (disjoint from the rows written above)
+  const int nloc = nloc_s;
+  for (int r = nloc + threadIdx.x; r < nslots; r += 1024) r2s[r] = -1;
+}
+
 // Token-major gather: x_perm[slot_to_row[t*k+j]] = x[t] for every hosted slot.
 // One wavefront per token. Each lane handles CPL 16-byte chunks of the row per pass, loaded together, so a
 // token costs one round trip for its slot map and its row, not one per chunk.
@@ -232,15 +334,21 @@ hipError_t launch_permute(const moe_desc& d, const int32_t* idx, const void* x, 
   const int nblk = (nslots + PM_SLOTS - 1) / PM_SLOTS;
   const int lc = d.local_count;
   int32_t* blk_counts = (int32_t*)ws;
-  {
-    KernelTimer kt("permute_hist", s);
-    hipLaunchKernelGGL(perm_hist_kernel, dim3(nblk), dim3(256), lc * sizeof(int), s, idx, nslots, d.local_begin, lc,
-                       blk_counts);
-  }
-  {
-    KernelTimer kt("permute_scatter", s);
-    hipLaunchKernelGGL(perm_scatter_kernel, dim3(nblk), dim3(256), 4 * lc * sizeof(int), s, idx, nslots,
-                       d.local_begin, lc, nbits_for(lc), nblk, blk_counts, counts, offsets, r2s, s2r);
+  if (nslots <= PS_MAX) {
+    KernelTimer kt("permute_sort", s);
+    hipLaunchKernelGGL(perm_sort_small_kernel, dim3(1), dim3(1024), PS_WAVES * lc * sizeof(int), s, idx, nslots,
+                       d.local_begin, lc, nbits_for(lc), counts, offsets, r2s, s2r);
+  } else {
+    {
+      KernelTimer kt("permute_hist", s);
+      hipLaunchKernelGGL(perm_hist_kernel, dim3(nblk), dim3(256), lc * sizeof(int), s, idx, nslots, d.local_begin,
+                         lc, blk_counts);
+    }
+    {
+      KernelTimer kt("permute_scatter", s);
+      hipLaunchKernelGGL(perm_scatter_kernel, dim3(nblk), dim3(256), 4 * lc * sizeof(int), s, idx, nslots,
+                         d.local_begin, lc, nbits_for(lc), nblk, blk_counts, counts, offsets, r2s, s2r);
+    }
   }
   {
     KernelTimer kt("permute_gather", s);
@@ -255,16 +363,19 @@ hipError_t launch_permute(const moe_desc& d, const int32_t* idx, const void* x, 
 
 // dx_t = sum_j dx_perm[row(t,j)] + sum_s dx_perm[T*k + s*T + t] (+ sum_e dlogits[t,e] * w_router[e])
 // One wavefront per token. The token's dlogits row is read once, together with its slot map; its nonzero
-// experts (k of them when the gate weights are renormalised) are found with ballots and only their router
-// rows are read, four experts' chunks at a time. Each lane handles CPL chunks of the row per pass; the
-// sums run in slot order, then shared experts, then experts in increasing index.
-template <typename T, int KM, int CPL>
+// experts (k of them when the gate weights are renormalised) are found with ballots. Each pass loads, in one
+// round trip, CPL chunks per lane of the token's KM routed rows, of up to SM shared-expert rows and of the router
+// rows of its first RB nonzero experts; further shared experts and nonzero experts follow in later round trips.
+// The sums run in slot order, then shared experts, then experts in increasing index.
+template <typename T, int KM, int SM, bool DL>
 __global__ __launch_bounds__(256) void unpermute_kernel(int Tn, int k, int S, int E, int cpr,
                                                         const Chunk* __restrict__ dxp,
                                                         const int32_t* __restrict__ s2r,
                                                         const float* __restrict__ dl,
                                                         const Chunk* __restrict__ wr, Chunk* __restrict__ dx) {
   constexpr int N = EPC<T>::value;
+  constexpr int RB = DL ? KM : 0;
+  constexpr int CPL = chunks_per_lane(KM + SM + RB);
   const int lane = threadIdx.x & 63;
   const int wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int nwaves = (gridDim.x * blockDim.x) >> 6;
@@ -274,23 +385,52 @@ __global__ __launch_bounds__(256) void unpermute_kernel(int Tn, int k, int S, in
 #pragma unroll
     for (int j = 0; j < KM; ++j) rows[j] = (j < k) ? s2r[(size_t)t * k + j] : -1;
     float g[4] = {0.f, 0.f, 0.f, 0.f};
-    uint64_t nz[4] = {0ull, 0ull, 0ull, 0ull};
-    if (dl) {
+    uint64_t rem[4] = {0ull, 0ull, 0ull, 0ull};
+    if (DL) {
 #pragma unroll
       for (int qq = 0; qq < 4; ++qq) {
         const int e = lane + 64 * qq;
         g[qq] = (e < E) ? dl[(size_t)t * E + e] : 0.f;
       }
 #pragma unroll
-      for (int qq = 0; qq < 4; ++qq) nz[qq] = __ballot(g[qq] != 0.f);
+      for (int qq = 0; qq < 4; ++qq) rem[qq] = __ballot(g[qq] != 0.f);
+    }
+    // the first RB nonzero experts in increasing order (wave-uniform), taken out of rem
+    int eb[RB > 0 ? RB : 1];
+    float gb[RB > 0 ? RB : 1];
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      eb[b] = -1;
+      gb[b] = 0.f;
+      const int qs = rem[0] ? 0 : rem[1] ? 1 : rem[2] ? 2 : rem[3] ? 3 : -1;
+      if (qs >= 0) {
+        const uint64_t m = qs == 0 ? rem[0] : qs == 1 ? rem[1] : qs == 2 ? rem[2] : rem[3];
+        const float gq = qs == 0 ? g[0] : qs == 1 ? g[1] : qs == 2 ? g[2] : g[3];
+        const int l = __builtin_ctzll(m);
+        eb[b] = l + 64 * qs;
+        gb[b] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gq), l));
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq)
+          if (qq == qs) rem[qq] &= rem[qq] - 1;
+      }
     }
     for (int c0 = lane; c0 < cpr; c0 += 64 * CPL) {
-      Chunk in[KM][CPL];
+      Chunk in[KM][CPL], sh[SM > 0 ? SM : 1][CPL], wb[RB > 0 ? RB : 1][CPL];
 #pragma unroll
       for (int j = 0; j < KM; ++j)
 #pragma unroll
         for (int u = 0; u < CPL; ++u)
           in[j][u] = (rows[j] >= 0 && c0 + 64 * u < cpr) ? dxp[(size_t)rows[j] * cpr + c0 + 64 * u] : zero_chunk();
+#pragma unroll
+      for (int s = 0; s < SM; ++s)
+#pragma unroll
+        for (int u = 0; u < CPL; ++u)
+          sh[s][u] = (c0 + 64 * u < cpr) ? dxp[(shared_base + (size_t)s * Tn + t) * cpr + c0 + 64 * u] : zero_chunk();
+#pragma unroll
+      for (int b = 0; b < RB; ++b)
+#pragma unroll
+        for (int u = 0; u < CPL; ++u)
+          wb[b][u] = (eb[b] >= 0 && c0 + 64 * u < cpr) ? wr[(size_t)eb[b] * cpr + c0 + 64 * u] : zero_chunk();
       float acc[CPL][N], v[N];
 #pragma unroll
       for (int u = 0; u < CPL; ++u) {
@@ -304,21 +444,38 @@ __global__ __launch_bounds__(256) void unpermute_kernel(int Tn, int k, int S, in
             for (int i = 0; i < N; ++i) acc[u][i] += v[i];
           }
         }
+#pragma unroll
+        for (int s = 0; s < SM; ++s) {
+          chunk_to_f<T>(sh[s][u], v);
+#pragma unroll
+          for (int i = 0; i < N; ++i) acc[u][i] += v[i];
+        }
       }
-      for (int sh = 0; sh < S; ++sh) {
+      for (int s = SM; s < S; ++s) {
 #pragma unroll
         for (int u = 0; u < CPL; ++u) {
           if (c0 + 64 * u < cpr) {
-            chunk_to_f<T>(dxp[(shared_base + (size_t)sh * Tn + t) * cpr + c0 + 64 * u], v);
+            chunk_to_f<T>(dxp[(shared_base + (size_t)s * Tn + t) * cpr + c0 + 64 * u], v);
 #pragma unroll
             for (int i = 0; i < N; ++i) acc[u][i] += v[i];
           }
         }
       }
 #pragma unroll
+      for (int b = 0; b < RB; ++b) {
+        if (eb[b] >= 0) {
+#pragma unroll
+          for (int u = 0; u < CPL; ++u) {
+            chunk_to_f<T>(wb[b][u], v);
+#pragma unroll
+            for (int i = 0; i < N; ++i) acc[u][i] = fmaf(gb[b], v[i], acc[u][i]);
+          }
+        }
+      }
+#pragma unroll
       for (int qq = 0; qq < 4; ++qq) {
-        uint64_t m = nz[qq];
-        while (m) {  // wave-uniform: up to four nonzero experts per round, in increasing order
+        uint64_t m = rem[qq];
+        while (m) {  // wave-uniform: the remaining nonzero experts, up to four per round, in increasing order
           int es[4];
           float ge[4];
 #pragma unroll
@@ -362,14 +519,17 @@ hipError_t launch_permute_bwd(const moe_desc& d, const void* dxp, const int32_t*
                               const void* wr, void* dx, hipStream_t s) {
   const int cpr = (int)(d.d_model * elem_bytes(d) / 16);
   KernelTimer kt("unpermute", s);
-  row_dispatch(d.top_k, cpr, [&](auto km, auto cpl) {
-    constexpr int KM = decltype(km)::value, CPL = decltype(cpl)::value;
+  batch_dispatch(d.top_k, d.n_shared, dl != nullptr, [&](auto km, auto sm, auto has_dl) {
+    constexpr int KM = decltype(km)::value, SM = decltype(sm)::value;
+    constexpr bool DL = decltype(has_dl)::value;
     if (d.dtype == MOE_BF16)
-      hipLaunchKernelGGL((unpermute_kernel<bf16, KM, CPL>), dim3(gather_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k,
-                         d.n_shared, d.n_experts, cpr, (const Chunk*)dxp, s2r, dl, (const Chunk*)wr, (Chunk*)dx);
+      hipLaunchKernelGGL((unpermute_kernel<bf16, KM, SM, DL>), dim3(gather_blocks(d.T)), dim3(256), 0, s, d.T,
+                         d.top_k, d.n_shared, d.n_experts, cpr, (const Chunk*)dxp, s2r, dl, (const Chunk*)wr,
+                         (Chunk*)dx);
     else
-      hipLaunchKernelGGL((unpermute_kernel<float, KM, CPL>), dim3(gather_blocks(d.T)), dim3(256), 0, s, d.T, d.top_k,
-                         d.n_shared, d.n_experts, cpr, (const Chunk*)dxp, s2r, dl, (const Chunk*)wr, (Chunk*)dx);
+      hipLaunchKernelGGL((unpermute_kernel<float, KM, SM, DL>), dim3(gather_blocks(d.T)), dim3(256), 0, s, d.T,
+                         d.top_k, d.n_shared, d.n_experts, cpr, (const Chunk*)dxp, s2r, dl, (const Chunk*)wr,
+                         (Chunk*)dx);
   });
   return hipGetLastError();
 }
