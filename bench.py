@@ -194,7 +194,7 @@ def hbm_steps(cfg, n_routed, kernels):
     """Achieved HBM bandwidth of the bandwidth-bound steps from their algorithmic bytes per launch
     (s = element bytes, N = routed rows, S = shared experts):
       router forward   T*d*s + E*d*s + 4*T*E + 8*T*k   (x and W_r read; logits, top-k indices and weights written)
-      permute          T*d*s + N*d*s + 8*T*k           (sort, or histogram and scatter, and gather launches together)
+      permute          T*d*s + N*d*s + 8*T*k           (histogram, scatter and gather launches together)
       combine          N*d*s + T*d*s + S*T*d*s + 8*T*k
       combine backward T*d*s + 2*N*d*s + 8*T*k
       unpermute        N*d*s + T*d*s + S*T*d*s + 4*T*k
@@ -204,19 +204,16 @@ def hbm_steps(cfg, n_routed, kernels):
     T, d, k, E, S, N = cfg.T, cfg.d, cfg.k, cfg.E, cfg.n_shared, n_routed
     table = {
         "route_fwd": (("route_fwd",), T * d * s + E * d * s + 4 * T * E + 8 * T * k),
-        "permute": (("permute_sort", "permute_hist", "permute_scatter", "permute_gather"),
-                    T * d * s + N * d * s + 8 * T * k),
+        "permute": (("permute_hist", "permute_scatter", "permute_gather"), T * d * s + N * d * s + 8 * T * k),
         "combine": (("combine",), N * d * s + T * d * s + S * T * d * s + 8 * T * k),
         "combine_bwd": (("combine_bwd",), T * d * s + 2 * N * d * s + 8 * T * k),
         "unpermute": (("unpermute",), N * d * s + T * d * s + S * T * d * s + 4 * T * k),
     }
     out = {}
     for step, (names, nbytes) in table.items():
-        # the permute is one sort launch (up to 16384 slots) or a histogram and a scatter launch, then the gather
-        launched = [n for n in names if n in kernels]
-        if not launched or (step == "permute" and "permute_gather" not in launched):
+        if not all(n in kernels for n in names):
             continue
-        us = sum(kernels[n]["avg_us"] for n in launched)
+        us = sum(kernels[n]["avg_us"] for n in names)
         gbs = nbytes / (us * 1e-6) / 1e9
         out[step] = {"bytes": nbytes, "us": round(us, 2), "GB/s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
     return out

@@ -3,7 +3,6 @@
 // and the hand-back of the input gradient (Sec. 3.2), summed per token.
 //
 // Ordering is reproducible bit for bit: rows of one expert are in increasing slot order.
-//   0. up to PS_MAX slots: histogram, scan and scatter in one workgroup (perm_sort_small_kernel); beyond:
 //   1. histogram: per block of PM_SLOTS slots, per hosted expert counts (LDS atomics; order-free)
 //   2. scatter: each block first derives its own base per expert from the histogram (the exclusive
 //      prefix over experts of the totals, plus the counts of the earlier blocks; block 0 also writes
@@ -54,6 +53,17 @@ __global__ __launch_bounds__(256) void perm_scatter_kernel(const int32_t* __rest
   __shared__ int nloc_s;
   __shared__ int part_before[256], part_tot[256];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  constexpr int ITERS = PM_SLOTS / 4 / 64;  // slots of a lane: a wave ranks its PM_SLOTS / 4 slots 64 at a time
+  const int a_w = blockIdx.x * PM_SLOTS + w * (PM_SLOTS / 4);
+  // the local expert of each of the lane's slots (-1: hosted elsewhere or past the end), loaded once, in flight
+  // together with the count-table loads below
+  int v_of[ITERS];
+#pragma unroll
+  for (int it = 0; it < ITERS; ++it) {
+    const int a = a_w + it * 64 + lane;
+    const int v = (a < nslots) ? idx[a] - lb : -1;
+    v_of[it] = (v >= 0 && v < lc) ? v : -1;
+  }
   for (int i = threadIdx.x; i < 4 * lc; i += 256) wcnt[i] = 0;
   {
     // Per expert, the rows of the earlier blocks and the total over all blocks. The nblk x lc count table is
@@ -105,17 +115,14 @@ __global__ __launch_bounds__(256) void perm_scatter_kernel(const int32_t* __rest
     }
   }
   __syncthreads();
-  const int a_w = blockIdx.x * PM_SLOTS + w * (PM_SLOTS / 4);
   const uint64_t lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
   int* mine = wcnt + w * lc;
   // pass 1: per-wave counts
-  for (int it = 0; it < PM_SLOTS / 4 / 64; ++it) {
-    const int a = a_w + it * 64 + lane;
-    int v = (a < nslots) ? idx[a] - lb : -1;
-    const bool loc = (v >= 0 && v < lc);
-    if (!loc) v = 0;
-    const uint64_t peers = peer_mask(v, loc, nbits);
-    if (loc && (peers & lt) == 0) mine[v] += __popcll(peers);
+#pragma unroll
+  for (int it = 0; it < ITERS; ++it) {
+    const int v = v_of[it];
+    const uint64_t peers = peer_mask(v < 0 ? 0 : v, v >= 0, nbits);
+    if (v >= 0 && (peers & lt) == 0) mine[v] += __popcll(peers);
   }
   __syncthreads();
   for (int e = threadIdx.x; e < lc; e += 256) {
@@ -128,114 +135,8 @@ __global__ __launch_bounds__(256) void perm_scatter_kernel(const int32_t* __rest
   }
   __syncthreads();
   // pass 2: stable ranks
-  for (int it = 0; it < PM_SLOTS / 4 / 64; ++it) {
-    const int a = a_w + it * 64 + lane;
-    int v = (a < nslots) ? idx[a] - lb : -1;
-    const bool loc = (v >= 0 && v < lc);
-    if (!loc) v = 0;
-    const uint64_t peers = peer_mask(v, loc, nbits);
-    int pos = 0;
-    if (loc) pos = mine[v] + __popcll(peers & lt);
-    if (a < nslots) {
-      if (loc) {
-        r2s[pos] = a;
-        s2r[a] = pos;
-      } else {
-        s2r[a] = -1;
-      }
-    }
-    if (loc && (peers & lt) == 0) mine[v] += __popcll(peers);
-  }
-  // rows beyond N_loc have no slot
-  const int nloc = nloc_s;
-  for (int i = threadIdx.x; i < PM_SLOTS; i += 256) {
-    int r = blockIdx.x * PM_SLOTS + i;
-    if (r < nslots && r >= nloc) r2s[r] = -1;
-  }
-}
-
-// Up to PS_MAX slots: the histogram, the scan and the stable scatter in one workgroup of 16 wavefronts, no
-// count table between launches. Wavefront w ranks slots [w * per_wave, (w + 1) * per_wave) in order, 64 at a
-// time, with the same peer-mask ballots as the scatter above; its per-expert bases follow the earlier wavefronts'
-// counts, so rows of one expert stay in increasing slot order.
-constexpr int PS_WAVES = 16, PS_ITERS = 16, PS_MAX = PS_WAVES * PS_ITERS * 64;
-
-__global__ __launch_bounds__(1024) void perm_sort_small_kernel(const int32_t* __restrict__ idx, int nslots, int lb,
-                                                               int lc, int nbits, int32_t* __restrict__ counts,
-                                                               int32_t* __restrict__ offsets,
-                                                               int32_t* __restrict__ r2s, int32_t* __restrict__ s2r) {
-  extern __shared__ int wcnt[];  // [PS_WAVES][lc]: per-wave counts, then per-wave first rows
-  __shared__ int tot_s[256], base_s[256];
-  __shared__ int nloc_s;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int per_wave = (nslots + PS_WAVES * 64 - 1) / (PS_WAVES * 64) * 64;  // a multiple of 64, <= 1024
-  const int a_w = w * per_wave;
-  for (int i = threadIdx.x; i < PS_WAVES * lc; i += 1024) wcnt[i] = 0;
-  int v_of[PS_ITERS];  // local expert of each of the lane's slots, -1 if hosted elsewhere or past the end
 #pragma unroll
-  for (int it = 0; it < PS_ITERS; ++it) {
-    const int a = a_w + it * 64 + lane;
-    int v = -1;
-    if (it * 64 < per_wave && a < nslots) {
-      v = idx[a] - lb;
-      if (v < 0 || v >= lc) v = -1;
-    }
-    v_of[it] = v;
-  }
-  __syncthreads();
-  const uint64_t lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
-  int* mine = wcnt + w * lc;
-  // pass 1: per-wave counts (the lowest lane of each peer group adds the group's size)
-#pragma unroll
-  for (int it = 0; it < PS_ITERS; ++it) {
-    if (it * 64 >= per_wave) break;  // wave-uniform
-    const int v = v_of[it];
-    const uint64_t peers = peer_mask(v < 0 ? 0 : v, v >= 0, nbits);
-    if (v >= 0 && (peers & lt) == 0) mine[v] += __popcll(peers);
-  }
-  __syncthreads();
-  // per expert: each wave's first row within the expert, and the expert's total
-  for (int e = threadIdx.x; e < lc; e += 1024) {
-    int r = 0;
-    for (int ww = 0; ww < PS_WAVES; ++ww) {
-      const int c = wcnt[ww * lc + e];
-      wcnt[ww * lc + e] = r;
-      r += c;
-    }
-    tot_s[e] = r;
-  }
-  __syncthreads();
-  // exclusive prefix of the totals over experts (lc <= 256), by the first wavefront
-  if (w == 0) {
-    int carry = 0;
-    for (int q = 0; q < 4; ++q) {
-      const int e = 64 * q + lane;
-      const int t = (e < lc) ? tot_s[e] : 0;
-      int incl = t;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const int o = __shfl_up(incl, off, 64);
-        if (lane >= off) incl += o;
-      }
-      if (e < lc) {
-        base_s[e] = carry + incl - t;
-        counts[e] = t;
-        offsets[e] = carry + incl - t;
-      }
-      carry += __shfl(incl, 63, 64);
-    }
-    if (lane == 0) {
-      offsets[lc] = carry;
-      nloc_s = carry;
-    }
-  }
-  __syncthreads();
-  for (int i = threadIdx.x; i < PS_WAVES * lc; i += 1024) wcnt[i] += base_s[i % lc];
-  __syncthreads();
-  // pass 2: stable ranks
-#pragma unroll
-  for (int it = 0; it < PS_ITERS; ++it) {
-    if (it * 64 >= per_wave) break;
+  for (int it = 0; it < ITERS; ++it) {
     const int a = a_w + it * 64 + lane;
     const int v = v_of[it];
     const uint64_t peers = peer_mask(v < 0 ? 0 : v, v >= 0, nbits);
@@ -250,9 +151,12 @@ __global__ __launch_bounds__(1024) void perm_sort_small_kernel(const int32_t* __
     }
     if (v >= 0 && (peers & lt) == 0) mine[v] += __popcll(peers);
   }
-  // rows beyond N_loc have no slot (disjoint from the rows written above)
+  // rows beyond N_loc have no slot
   const int nloc = nloc_s;
-  for (int r = nloc + threadIdx.x; r < nslots; r += 1024) r2s[r] = -1;
+  for (int i = threadIdx.x; i < PM_SLOTS; i += 256) {
+    int r = blockIdx.x * PM_SLOTS + i;
+    if (r < nslots && r >= nloc) r2s[r] = -1;
+  }
 }
 
 // Token-major gather: x_perm[slot_to_row[t*k+j]] = x[t] for every hosted slot.
@@ -334,21 +238,15 @@ hipError_t launch_permute(const moe_desc& d, const int32_t* idx, const void* x, 
   const int nblk = (nslots + PM_SLOTS - 1) / PM_SLOTS;
   const int lc = d.local_count;
   int32_t* blk_counts = (int32_t*)ws;
-  if (nslots <= PS_MAX) {
-    KernelTimer kt("permute_sort", s);
-    hipLaunchKernelGGL(perm_sort_small_kernel, dim3(1), dim3(1024), PS_WAVES * lc * sizeof(int), s, idx, nslots,
-                       d.local_begin, lc, nbits_for(lc), counts, offsets, r2s, s2r);
-  } else {
-    {
-      KernelTimer kt("permute_hist", s);
-      hipLaunchKernelGGL(perm_hist_kernel, dim3(nblk), dim3(256), lc * sizeof(int), s, idx, nslots, d.local_begin,
-                         lc, blk_counts);
-    }
-    {
-      KernelTimer kt("permute_scatter", s);
-      hipLaunchKernelGGL(perm_scatter_kernel, dim3(nblk), dim3(256), 4 * lc * sizeof(int), s, idx, nslots,
-                         d.local_begin, lc, nbits_for(lc), nblk, blk_counts, counts, offsets, r2s, s2r);
-    }
+  {
+    KernelTimer kt("permute_hist", s);
+    hipLaunchKernelGGL(perm_hist_kernel, dim3(nblk), dim3(256), lc * sizeof(int), s, idx, nslots, d.local_begin, lc,
+                       blk_counts);
+  }
+  {
+    KernelTimer kt("permute_scatter", s);
+    hipLaunchKernelGGL(perm_scatter_kernel, dim3(nblk), dim3(256), 4 * lc * sizeof(int), s, idx, nslots,
+                       d.local_begin, lc, nbits_for(lc), nblk, blk_counts, counts, offsets, r2s, s2r);
   }
   {
     KernelTimer kt("permute_gather", s);
