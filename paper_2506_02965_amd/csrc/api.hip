@@ -132,7 +132,7 @@ KernelTimer::KernelTimer(const char* n, hipStream_t s) : name(n), stream(s), slo
   }
   hipEvent_t a = ts.pool[2 * ts.used], b = ts.pool[2 * ts.used + 1];
   ++ts.used;
-  hipEventRecord(a, s);
+  (void)hipEventRecord(a, s);
   ts.recs.push_back({n, a, b});  // within the reserved capacity
   slot = (void*)(uintptr_t)ts.recs.size();
 }
@@ -141,7 +141,7 @@ KernelTimer::~KernelTimer() {
   TimingState& ts = timing();
   std::lock_guard<std::mutex> lk(ts.mu);
   size_t i = (size_t)(uintptr_t)slot - 1;
-  if (i < ts.recs.size()) hipEventRecord(ts.recs[i].b, stream);
+  if (i < ts.recs.size()) (void)hipEventRecord(ts.recs[i].b, stream);
 }
 }  // namespace pcmoe
 

@@ -12,8 +12,10 @@
 //     the way into registers by ds_read_b64_tr_b16 (two reads per MFMA operand);
 //   * 256 x 256 tiles with 16 wavefronts (4 x 4, 64 x 64 each) by default, 192 x 256 tiles with 8
 //     wavefronts for a single-round down projection, 128 x 128 tiles with 4 when a side is not a multiple
-//     of 256; fp32 accumulators, per-wave epilogue staged through LDS in fp32 and written as 16-byte
-//     chunks (SwiGLU and its adjoint fused);
+//     of 256; for d_model >= 4096, a software-pipelined 256 x 256 tile with 4 wavefronts (one per SIMD,
+//     128 x 128 each, accumulators in AGPRs, 32-deep K-tiles in a 4-stage ring) for every contraction but
+//     the down projection; fp32 accumulators, per-wave epilogue staged through LDS in fp32 and written as
+//     16-byte chunks (SwiGLU and its adjoint fused);
 //   * tiles decoded on the device from a plan of m-tile prefixes (grouped_gemm.h); independent
 //     contractions of the backward share one launch (gemm_bf16_pair_kernel).
 #include "grouped_gemm.h"
@@ -96,6 +98,17 @@ __device__ __forceinline__ Chunk lds_kc_pair(const char* chunk, int q) {
   return c;
 }
 
+// The whole 16-byte chunk in one read, in k order (the pipelined one-wavefront-per-SIMD tiles).
+__device__ __forceinline__ Chunk lds_kc_whole(const char* chunk) {
+  const uint4 v = *reinterpret_cast<const uint4*>(chunk);
+  Chunk c;
+  c.w[0] = v.x;
+  c.w[1] = v.y;
+  c.w[2] = v.z;
+  c.w[3] = v.w;
+  return c;
+}
+
 __device__ __forceinline__ Chunk lds_tr_pair(const char* a0, const char* a1) {
   typedef __attribute__((address_space(3))) short4v* lp;
   short4v r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lp)(a0));
@@ -108,6 +121,16 @@ __device__ __forceinline__ Chunk lds_tr_pair(const char* a0, const char* a1) {
   return c;
 }
 
+// The same MFMA with its accumulator pinned to AGPRs and updated in place. With 256 accumulator registers per
+// lane, the compiler's own choice writes some results to other registers and then moves every accumulator
+// around the loop. Reads of the result by anything but the next MFMA on the same accumulator follow only after
+// the K loop (and its trailing s_nops). Volatile: the MFMAs keep their order relative to the direct loads and
+// barriers they are interleaved with (the scheduler would otherwise bunch the loads together).
+__device__ __forceinline__ void mfma_bf16_agpr(floatx4& acc, const Chunk& a, const Chunk& b) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0"
+      : "+a"(acc)
+      : "v"(__builtin_bit_cast(int32x4, a)), "v"(__builtin_bit_cast(int32x4, b)));
+}
 __device__ __forceinline__ void mfma_bf16(floatx4& acc, const Chunk& a, const Chunk& b) {
   acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), acc, 0,
                                                 0, 0);
@@ -147,6 +170,10 @@ struct Cfg2 {
   static constexpr int IA = BM * ROWB / 1024 / NW;  // direct loads per wave per K-tile (1 KB each)
   static constexpr int IB = BN * ROWB / 1024 / NW;
   static constexpr int LOADS = IA + IB;
+  // 256 x 256 tiles with 4 wavefronts (one per SIMD, 128 x 128 each, 256 accumulator registers): the
+  // software-pipelined K loop, and a kernel that may use all 512 registers of a lane
+  static constexpr bool PIPE = NW == 4 && BM == 256 && BN == 256;
+  static constexpr int WAVES_PER_EU = PIPE ? 1 : (NW >= 4 ? NW / 4 : 1);
   static_assert(IA * 1024 * NW == BM * ROWB && IB * 1024 * NW == BN * ROWB, "tiles must split evenly over waves");
 };
 
@@ -176,43 +203,36 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
 
   // ------------------------------------------------------------------ operand sources
   // A (M side). Ragged kinds: K-contiguous rows of the group; weight gradients: [rows][M] (K-major).
-  int32x4 ra;
-  int a_ld;  // bytes between consecutive rows in memory
-  {
-    const char* base;
-    if (KIND == FWD_GU) { base = routed ? (const char*)p.xp + rs * d * ES : (const char*)p.x; a_ld = d * ES; }
-    else if (KIND == FWD_DOWN) { base = (const char*)p.h + rs * f * ES; a_ld = f * ES; }
-    else if (KIND == BWD_DH || KIND == WG_DOWN) {
-      base = routed ? (const char*)p.dyp + rs * d * ES : (const char*)p.dy;
-      a_ld = d * ES;
-    } else { base = (const char*)p.dgu + rs * 2 * f * ES; a_ld = 2 * f * ES; }
-    ra = make_rsrc(base, (uint32_t)((size_t)rows * a_ld));
-  }
-  // B (N side)
-  int32x4 rb0, rb1;  // rb1: W_up (FWD_GU rows of the up half; BWD_DX K rows >= f)
-  int b_ld;
-  if (KIND == FWD_GU) {
-    rb0 = make_rsrc((const char*)p.wg + (size_t)g * f * d * ES, (uint32_t)((size_t)f * d * ES));
-    rb1 = make_rsrc((const char*)p.wu + (size_t)g * f * d * ES, (uint32_t)((size_t)f * d * ES));
+  // B (N side); B1: W_up (FWD_GU rows of the up half; BWD_DX K rows >= f). Each as a base and a byte range.
+  const char *a_base, *b0_base, *b1_base;
+  uint32_t a_bytes, b_bytes;
+  int a_ld, b_ld;  // bytes between consecutive rows in memory
+  if (KIND == FWD_GU) { a_base = routed ? (const char*)p.xp + rs * d * ES : (const char*)p.x; a_ld = d * ES; }
+  else if (KIND == FWD_DOWN) { a_base = (const char*)p.h + rs * f * ES; a_ld = f * ES; }
+  else if (KIND == BWD_DH || KIND == WG_DOWN) {
+    a_base = routed ? (const char*)p.dyp + rs * d * ES : (const char*)p.dy;
+    a_ld = d * ES;
+  } else { a_base = (const char*)p.dgu + rs * 2 * f * ES; a_ld = 2 * f * ES; }
+  a_bytes = (uint32_t)((size_t)rows * a_ld);
+  if (KIND == FWD_GU || KIND == BWD_DX) {
+    b0_base = (const char*)p.wg + (size_t)g * f * d * ES;
+    b1_base = (const char*)p.wu + (size_t)g * f * d * ES;
+    b_bytes = (uint32_t)((size_t)f * d * ES);
     b_ld = d * ES;
   } else if (KIND == FWD_DOWN || KIND == BWD_DH) {
-    rb0 = make_rsrc((const char*)p.wd + (size_t)g * d * f * ES, (uint32_t)((size_t)d * f * ES));
-    rb1 = rb0;
+    b0_base = b1_base = (const char*)p.wd + (size_t)g * d * f * ES;
+    b_bytes = (uint32_t)((size_t)d * f * ES);
     b_ld = f * ES;
-  } else if (KIND == BWD_DX) {
-    rb0 = make_rsrc((const char*)p.wg + (size_t)g * f * d * ES, (uint32_t)((size_t)f * d * ES));
-    rb1 = make_rsrc((const char*)p.wu + (size_t)g * f * d * ES, (uint32_t)((size_t)f * d * ES));
-    b_ld = d * ES;
   } else if (KIND == WG_DOWN) {
-    rb0 = make_rsrc((const char*)p.h + rs * f * ES, (uint32_t)((size_t)rows * f * ES));
-    rb1 = rb0;
+    b0_base = b1_base = (const char*)p.h + rs * f * ES;
+    b_bytes = (uint32_t)((size_t)rows * f * ES);
     b_ld = f * ES;
   } else {  // WG_GU
-    const char* base = routed ? (const char*)p.xp + rs * d * ES : (const char*)p.x;
-    rb0 = make_rsrc(base, (uint32_t)((size_t)rows * d * ES));
-    rb1 = rb0;
+    b0_base = b1_base = routed ? (const char*)p.xp + rs * d * ES : (const char*)p.x;
+    b_bytes = (uint32_t)((size_t)rows * d * ES);
     b_ld = d * ES;
   }
+  const int32x4 ra = make_rsrc(a_base, a_bytes), rb0 = make_rsrc(b0_base, b_bytes), rb1 = make_rsrc(b1_base, b_bytes);
 
   // K-major operands in the padded layout (mk_row); a 128-wide wave tile reads two of its 64-column blocks
   constexpr bool MKP_A = !KT::a_kc && BM == 256 && (C::WTM == 64 || C::WTM == 128);
@@ -295,45 +315,54 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
   // only the columns past N, which are neither computed nor stored.
   const bool wave_cols = n0 + wn * C::WTN < p.n_extent;  // wave-uniform
 
-  // The operand fragments of MFMA k-step kk (32 deep) of the K-tile in stage `st`.
+  // Operand fragments of MFMA k-step kk (32 deep) of the K-tile whose stage starts at As (A) / Bs (B).
+  // K-contiguous fragments: row 16 * i + li of the wave's rows; the swizzle sees only li, and fragment i sits FRAG
+  // bytes after fragment 0 (an immediate offset of the LDS read). Odd lane groups take k-elements 4..7 before
+  // 0..3 (lds_kc_pair), and the transposed reads of the partner operand follow the same order (SW = 1); with it
+  // the transposed reads of the padded layout hit 8 distinct bank groups per pass. The pipelined tiles read a
+  // K-contiguous fragment whole and in k order (SW = 0: one LDS instruction per fragment, which measured faster
+  // there), at the cost of 2-way bank conflicts in the transposed reads of the contractions that mix both kinds.
+  constexpr int FRAG = 16 * C::ROWB + 16;
+  constexpr int SW = (C::PIPE && (KT::a_kc || KT::b_kc)) ? 0 : 1;
+  // padded K-major fragments: the lane's two k-rows (kl1, kl2) and its 8-byte column group; fragment i of a wave
+  // tile lies in 64-column block (wave offset + 16 i) / 64, at 32 (i mod 4) bytes
+  const int kl1 = 8 * q + 4 * SW * (q & 1) + (li >> 2), kl2 = kl1 + 4 - 8 * SW * (q & 1);
+  const auto mk_lane = [&](int kl, int w, int kk) {
+    return mk_row(kl) + 128 * ((w + (kl & 1)) & 3) + 16 * ((li & 3) >> 1) + 8 * (li & 1) + 16 * MK_BLOCK * kk;
+  };
+  const auto frag_a = [&](const char* As, int kk, int i) {
+    if (KT::a_kc) {
+      const int lane_kc = li * C::ROWB + (((4 * kk + q) ^ kc_swz<BK>(li)) << 4);
+      const char* ch = As + kc_row<C::ROWB>(wm * C::WTM) + lane_kc + i * FRAG;
+      return C::PIPE ? lds_kc_whole(ch) : lds_kc_pair(ch, q);
+    } else if (MKP_A) {
+      const int w = (wm * C::WTM) / 64 + i / 4;
+      return lds_tr_pair(As + mk_lane(kl1, w, kk) + 32 * (i % 4), As + mk_lane(kl2, w, kk) + 32 * (i % 4));
+    } else {
+      const int k1 = 32 * kk + kl1, k2 = 32 * kk + kl2, mn = wm * C::WTM + 16 * i + 4 * (li & 3);
+      return lds_tr_pair(As + k1 * (BM * 2) + (((mn >> 3) ^ mc_swz(k1)) << 4) + (mn & 7) * 2,
+                         As + k2 * (BM * 2) + (((mn >> 3) ^ mc_swz(k2)) << 4) + (mn & 7) * 2);
+    }
+  };
+  const auto frag_b = [&](const char* Bs, int kk, int j) {
+    if (KT::b_kc) {
+      const int lane_kc = li * C::ROWB + (((4 * kk + q) ^ kc_swz<BK>(li)) << 4);
+      const char* ch = Bs + kc_row<C::ROWB>(wn * C::WTN) + lane_kc + j * FRAG;
+      return C::PIPE ? lds_kc_whole(ch) : lds_kc_pair(ch, q);
+    } else if (MKP_B) {
+      const int w = (wn * C::WTN) / 64 + j / 4;
+      return lds_tr_pair(Bs + mk_lane(kl1, w, kk) + 32 * (j % 4), Bs + mk_lane(kl2, w, kk) + 32 * (j % 4));
+    } else {
+      const int k1 = 32 * kk + kl1, k2 = 32 * kk + kl2, mn = wn * C::WTN + 16 * j + 4 * (li & 3);
+      return lds_tr_pair(Bs + k1 * (BN * 2) + (((mn >> 3) ^ mc_swz(k1)) << 4) + (mn & 7) * 2,
+                         Bs + k2 * (BN * 2) + (((mn >> 3) ^ mc_swz(k2)) << 4) + (mn & 7) * 2);
+    }
+  };
   const auto read_frags = [&](const char* As, const char* Bs, int kk, Chunk (&a)[C::FM], Chunk (&b)[C::FN]) {
-    // K-contiguous fragments: row 16 * i + li of the wave's rows; the swizzle sees only li, and
-    // fragment i sits FRAG bytes after fragment 0 (an immediate offset of the LDS read)
-    constexpr int FRAG = 16 * C::ROWB + 16;
-    const int lane_kc = li * C::ROWB + (((4 * kk + q) ^ kc_swz<BK>(li)) << 4);
-    // padded K-major fragments: the lane's two k-rows (kl1, kl2) and its 8-byte column group; fragment i of a
-    // wave tile lies in 64-column block (wave offset + 16 i) / 64, at 32 (i mod 4) bytes
-    const int kl1 = 8 * q + 4 * (q & 1) + (li >> 2), kl2 = kl1 + 4 - 8 * (q & 1);
-    const int lane_mk = 16 * ((li & 3) >> 1) + 8 * (li & 1) + 16 * MK_BLOCK * kk;
-    const auto mk_lane = [&](int kl, int w) { return mk_row(kl) + 128 * ((w + (kl & 1)) & 3) + lane_mk; };
 #pragma unroll
-    for (int i = 0; i < C::FM; ++i) {
-      if (KT::a_kc) {
-        a[i] = lds_kc_pair(As + kc_row<C::ROWB>(wm * C::WTM) + lane_kc + i * FRAG, q);
-      } else if (MKP_A) {
-        const int w = (wm * C::WTM) / 64 + i / 4;
-        a[i] = lds_tr_pair(As + mk_lane(kl1, w) + 32 * (i % 4), As + mk_lane(kl2, w) + 32 * (i % 4));
-      } else {
-        const int k1 = 32 * kk + 8 * q + 4 * (q & 1) + (li >> 2), mn = wm * C::WTM + 16 * i + 4 * (li & 3);
-        const int k2 = k1 + 4 - 8 * (q & 1);
-        a[i] = lds_tr_pair(As + k1 * (BM * 2) + (((mn >> 3) ^ mc_swz(k1)) << 4) + (mn & 7) * 2,
-                           As + k2 * (BM * 2) + (((mn >> 3) ^ mc_swz(k2)) << 4) + (mn & 7) * 2);
-      }
-    }
+    for (int i = 0; i < C::FM; ++i) a[i] = frag_a(As, kk, i);
 #pragma unroll
-    for (int j = 0; j < C::FN; ++j) {
-      if (KT::b_kc) {
-        b[j] = lds_kc_pair(Bs + kc_row<C::ROWB>(wn * C::WTN) + lane_kc + j * FRAG, q);
-      } else if (MKP_B) {
-        const int w = (wn * C::WTN) / 64 + j / 4;
-        b[j] = lds_tr_pair(Bs + mk_lane(kl1, w) + 32 * (j % 4), Bs + mk_lane(kl2, w) + 32 * (j % 4));
-      } else {
-        const int k1 = 32 * kk + 8 * q + 4 * (q & 1) + (li >> 2), mn = wn * C::WTN + 16 * j + 4 * (li & 3);
-        const int k2 = k1 + 4 - 8 * (q & 1);
-        b[j] = lds_tr_pair(Bs + k1 * (BN * 2) + (((mn >> 3) ^ mc_swz(k1)) << 4) + (mn & 7) * 2,
-                           Bs + k2 * (BN * 2) + (((mn >> 3) ^ mc_swz(k2)) << 4) + (mn & 7) * 2);
-      }
-    }
+    for (int j = 0; j < C::FN; ++j) b[j] = frag_b(Bs, kk, j);
   };
 
   // Every wave loads IA + IB instructions of each K-tile (instruction jj = wave + NW j) and reads its fragments
@@ -350,6 +379,109 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
 #pragma unroll
     for (int j = 0; j < C::IB; ++j) load_b(kt, stage, wave + C::NW * j, vb[j], bup[j]);
   };
+  if constexpr (C::PIPE) {
+    // One wavefront per SIMD (4 wavefronts of 128 x 128): no other wavefront hides a stall of this one, so the
+    // K loop is software-pipelined by hand. 32-deep K-tiles in a 4-stage ring; a K-tile's fragments are read into
+    // registers during the step before the one that multiplies them, so its stage is free again from that step's
+    // end. In the step of K-tile kt:
+    //   * MFMAs 0..15 of kt;
+    //   * the wait for this wave's loads of K-tile kt + 1 and a workgroup barrier: every wave's loads of kt + 1
+    //     have landed, and every wave has read K-tile kt (so its stage is free);
+    //   * MFMAs 16..63 of kt, with the 16 fragment reads of kt + 1 (into the other register set, in the order the
+    //     next step uses them) and the 8 direct loads of K-tile kt + 4 (into kt's stage) between them.
+    // A load has three steps to land before the barrier that waits for it.
+    // Every instruction of the step keeps this order (the MFMAs and the loads are volatile asm, the reads cannot
+    // cross them). Nothing in the step branches: a branch around MFMAs makes the compiler copy all 256
+    // accumulators. So the loop runs an even number of steps (K-tiles past K are zeros: only the weight
+    // gradients, whose K rows end at the group's end, can have an odd count), and the loads of K-tiles past the
+    // last one are issued with an offset past every buffer range (they return zeros and fetch nothing). A
+    // wavefront with no rows or no columns to compute takes the same loads and barriers without MFMAs and
+    // fragment reads, and then returns.
+    static_assert(STAGES == 4 && C::KK == 1 && C::IA == 4 && C::IB == 4 && C::FM == 8 && C::FN == 8,
+                  "pipelined tile");
+    const int KTN2 = (KTN + 1) & ~1;
+    constexpr int OOR = 0x7fffffff;  // no operand range reaches 2^31 bytes
+    // load l (0..7, a constant after unrolling) of K-tile kt: one direct load whatever kt, so that nothing branches
+    const auto load_one = [&](int kt, int l) {
+      const bool live = kt < KTN;
+      const int k0 = kt * BK;
+      const uint32_t st = lds_base + (kt & 3) * C::STAGE_BYTES;
+      if (l < C::IA) {
+        const int jj = wave + C::NW * l;
+        const int off = va[l & (C::IA - 1)] + (KT::a_kc ? k0 * ES : k0 * a_ld);
+        dma16(ra, st + jj * 1024 + pad(jj, KT::a_kc, MKP_A), live ? off : OOR);
+      } else {
+        const int j = (l - C::IA) & (C::IB - 1), jj = wave + C::NW * j;
+        int off;
+        int32x4 rsrc;
+        if (KIND == BWD_DX) {
+          const bool hi = k0 >= f;  // K rows >= f are W_up rows
+          rsrc = hi ? rb1 : rb0;
+          off = vb[j] + (hi ? k0 - f : k0) * b_ld;
+        } else {
+          rsrc = bup[j] ? rb1 : rb0;
+          off = vb[j] + (KT::b_kc ? k0 * ES : k0 * b_ld);
+        }
+        dma16(rsrc, st + C::A_BYTES + jj * 1024 + pad(jj, KT::b_kc, MKP_B), live ? off : OOR);
+      }
+    };
+    const auto issue_all = [&](int kt) {
+#pragma unroll
+      for (int l = 0; l < 8; ++l) load_one(kt, l);
+    };
+    const auto barrier = [] { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
+    issue_all(0);
+    issue_all(1);
+    issue_all(2);
+    issue_all(3);
+    wait_vmcnt<24>();  // K-tile 0 has landed
+    barrier();
+    if (!wave_rows || !wave_cols) {
+      for (int kt = 0; kt < KTN2; ++kt) {
+        wait_vmcnt<16>();  // K-tile kt + 1 has landed (kt + 2 and kt + 3 may be in flight)
+        barrier();
+        issue_all(kt + 4);
+      }
+      wait_vmcnt<0>();
+      __syncthreads();
+      return;
+    }
+    Chunk fa[2][C::FM], fb[2][C::FN];
+    read_frags(smem, smem + C::A_BYTES, 0, fa[0], fb[0]);
+    // the step of K-tile kt with its fragments in register set S
+    const auto step = [&](int kt, auto set) {
+      constexpr int S = decltype(set)::value;
+      const char* As = smem + ((kt + 1) & 3) * C::STAGE_BYTES;
+#pragma unroll
+      for (int i = 0; i < C::FM; ++i) {
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j) {
+          const int m = i * C::FN + j;
+          if (m == 16) {
+            wait_vmcnt<16>();  // K-tile kt + 1 has landed (kt + 2 and kt + 3 may be in flight)
+            barrier();
+          }
+          mfma_bf16_agpr(acc[i][j], fa[S][i], fb[S][j]);
+          if (m >= 16) {
+            const int r = m - 16;  // 0..47: a read after every third MFMA, a load after every sixth
+            if (r % 3 == 0) {
+              const int t = r / 3;  // fa[0], fb[0..7], fa[1..7]
+              if (t == 0) fa[S ^ 1][0] = frag_a(As, 0, 0);
+              else if (t <= 8) fb[S ^ 1][t - 1] = frag_b(As + C::A_BYTES, 0, t - 1);
+              else fa[S ^ 1][t - 8] = frag_a(As, 0, t - 8);
+            }
+            if (r % 6 == 2) load_one(kt + 4, r / 6);
+          }
+        }
+      }
+    };
+    for (int kt = 0; kt < KTN2; kt += 2) {
+      step(kt, std::integral_constant<int, 0>{});
+      step(kt + 1, std::integral_constant<int, 1>{});
+    }
+    wait_vmcnt<0>();  // the zero-filling loads past the last K-tile land before the epilogue reuses the LDS
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");  // the last MFMAs' results are ready to read
+  } else {
   // prologue: STAGES-1 tiles in flight
 #pragma unroll
   for (int s = 0; s < STAGES - 1; ++s)
@@ -375,6 +507,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
 #pragma unroll
         for (int j = 0; j < C::FN; ++j) mfma_bf16(acc[i][j], a[i], b[j]);
     }
+  }
   }
   __syncthreads();  // every wave is done with the operand buffers
 
@@ -467,7 +600,8 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
 }
 
 template <int BM, int BN, int BK, int KIND, int STAGES, int WM, int WN>
-__global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs p) {
+__global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(
+    Cfg2<BM, BN, BK, STAGES, WM, WN>::WAVES_PER_EU))) void gemm_bf16_kernel(GemmArgs p) {
   extern __shared__ __align__(16) char smem[];
   gemm_tile<BM, BN, BK, KIND, STAGES, WM, WN>(p, blockIdx.x, smem);
 }
@@ -476,7 +610,9 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs p) {
 // K loops, so they start first), the rest tiles of KB. The CUs that KA's tile grid leaves idle
 // work through KB meanwhile, instead of idling until the next launch.
 template <int BM, int BN, int BK, int KA, int KB, int STAGES, int WM, int WN>
-__global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_pair_kernel(GemmArgs pa, GemmArgs pb, int grid_a) {
+__global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(
+    Cfg2<BM, BN, BK, STAGES, WM, WN>::WAVES_PER_EU))) void gemm_bf16_pair_kernel(GemmArgs pa, GemmArgs pb,
+                                                                                 int grid_a) {
   extern __shared__ __align__(16) char smem[];
   const int bid = blockIdx.x;
   if (bid < grid_a) gemm_tile<BM, BN, BK, KA, STAGES, WM, WN>(pa, bid, smem);
@@ -505,12 +641,12 @@ static hipError_t run2(const GemmArgs& a, long tiles, hipStream_t s, const char*
 // 192-row tiles (K-contiguous A only: the row-ragged contractions) serve a contraction whose 256-row grid is
 // one partial round of the chip.
 enum TileShape { T128x128s2 = 0, T256x128w8, T128x256w8, T256x256w8, T256x256k32, T256x128k32, T128x128k32,
-                 T256x256w16, T256x256w16k32s4, T256x256w16k32s3, T192x256w8, N_SHAPES };
-static const int kShapeBM[N_SHAPES] = {128, 256, 128, 256, 256, 256, 128, 256, 256, 256, 192};
-static const int kShapeBN[N_SHAPES] = {128, 128, 256, 256, 256, 128, 128, 256, 256, 256, 256};
+                 T256x256w16, T256x256w16k32s4, T256x256w16k32s3, T192x256w8, T256x256w4, N_SHAPES };
+static const int kShapeBM[N_SHAPES] = {128, 256, 128, 256, 256, 256, 128, 256, 256, 256, 192, 256};
+static const int kShapeBN[N_SHAPES] = {128, 128, 256, 256, 256, 128, 128, 256, 256, 256, 256, 256};
 static const char* kShapeName[N_SHAPES] = {"128x128s2", "256x128w8", "128x256w8", "256x256w8", "256x256k32",
                                            "256x128k32", "128x128k32", "256x256w16", "256x256w16k32s4",
-                                           "256x256w16k32s3", "192x256w8"};
+                                           "256x256w16k32s3", "192x256w8", "256x256w4"};
 
 static const char* kKindName[6] = {"gemm_fwd_gate_up", "gemm_fwd_down", "gemm_bwd_dh", "gemm_bwd_dx",
                                    "gemm_wgrad_down", "gemm_wgrad_gate_up"};
@@ -544,6 +680,7 @@ static hipError_t run_shape(int shape, const GemmArgs& a, long tiles, hipStream_
     case T256x256w16: return run2<256, 256, 64, KIND, 2, 4, 4>(a, tiles, s, kKindName[KIND]);
     case T256x256w16k32s4: return run2<256, 256, 32, KIND, 4, 4, 4>(a, tiles, s, kKindName[KIND]);
     case T256x256w16k32s3: return run2<256, 256, 32, KIND, 3, 4, 4>(a, tiles, s, kKindName[KIND]);
+    case T256x256w4: return run2<256, 256, 32, KIND, 4, 2, 2>(a, tiles, s, kKindName[KIND]);
     case T192x256w8:
       if constexpr (KindTraits<KIND>::a_kc) return run2<192, 256, 64, KIND, 2, 2, 4>(a, tiles, s, kKindName[KIND]);
       return hipErrorInvalidValue;  // not selected for K-major A (fit_shape)
@@ -576,11 +713,18 @@ static int tile_shape(int kind, const moe_desc& d) {
   // FWD_DOWN (N = d_model): when its 256x256 grid is one partial round of the chip, 192-row tiles still fit one
   // round and each costs about 3/4 of a 256-row tile. (The backward kinds run paired with a weight gradient,
   // which shares their shape.)
-  if (kind == FWD_DOWN && d.d_model % 256 == 0) {
-    const long n = d.d_model / 256;
-    if (mtile_bound2(d, 256) * n <= device_cus() && mtile_bound2(d, 192) * n <= device_cus()) return T192x256w8;
+  if (kind == FWD_DOWN) {
+    if (d.d_model % 256 == 0) {
+      const long n = d.d_model / 256;
+      if (mtile_bound2(d, 256) * n <= device_cus() && mtile_bound2(d, 192) * n <= device_cus()) return T192x256w8;
+    }
+    return T256x256w16;
   }
-  return T256x256w16;
+  // The pipelined 4-wavefront tile pays off on long K loops only: its prologue and epilogue (one wavefront per
+  // SIMD, each storing four times the outputs of a 16-wavefront tile's wavefront) are amortised over K. Measured:
+  // 1.6% faster per layer step at d_model = 4096 (the dX + dW_gate|up pair 3.4%), equal at d_model = 2048 with
+  // 64 experts, 3% slower for a 16-expert shard at d_model = 2048 and 7% slower at d_model = 1024.
+  return d.d_model >= 4096 ? T256x256w4 : T256x256w16;
 }
 
 // Upper bound on the m-tiles of the row-ragged kinds (per-expert counts stay on the device).
@@ -661,10 +805,10 @@ static int device_cus() {
 static int fit_shape(int sh, int M, int N) {
   int bm = kShapeBM[sh], bn = kShapeBN[sh];
   if (M > 0 && (M % bm || bm == 192)) bm = 128;  // weight gradients (K-major A) take no 192-row tiles
-  if (N % bn && !(sh == T256x256w16 && N % 128 == 0)) bn = 128;
+  if (N % bn && !((sh == T256x256w16 || sh == T256x256w4) && N % 128 == 0)) bn = 128;
   if (bm == kShapeBM[sh] && bn == kShapeBN[sh]) return sh;
   const bool k32 = sh == T256x256k32 || sh == T256x128k32 || sh == T128x128k32;
-  if (sh == T256x256w16 || sh == T256x256w16k32s4 || sh == T256x256w16k32s3)
+  if (sh == T256x256w16 || sh == T256x256w16k32s4 || sh == T256x256w16k32s3 || sh == T256x256w4)
     return T128x128s2;  // measured best when one side must drop to 128
   if (bm == 256 && bn == 128) return k32 ? T256x128k32 : T256x128w8;
   if (bm == 128 && bn == 256) return T128x256w8;
@@ -734,6 +878,7 @@ static hipError_t run_pair(const Prep& A, const Prep& B, hipStream_t s, const ch
   if (A.sh == B.sh && pair_enabled()) {
     switch (A.sh) {
       case T256x256w16: return run_pair2<256, 256, 64, KA, KB, 2, 4, 4>(A.a, A.tiles, B.a, B.tiles, s, name);
+      case T256x256w4: return run_pair2<256, 256, 32, KA, KB, 4, 2, 2>(A.a, A.tiles, B.a, B.tiles, s, name);
       case T128x128s2: return run_pair2<128, 128, 64, KA, KB, 2, 2, 2>(A.a, A.tiles, B.a, B.tiles, s, name);
       default: break;
     }
