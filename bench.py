@@ -219,6 +219,33 @@ def hbm_steps(cfg, n_routed, kernels):
     return out
 
 
+def dense_reference(cfg, steps=20):
+    """Context, not a target: the vendor's dense bf16 GEMM (torch.matmul, i.e. hipBLASLt) on the workload's expert
+    contractions with all routed rows as one dense matrix (forward gate|up, forward down, input gradient dX).
+    TFLOP/s per shape, timed with HIP events on random bf16 operands."""
+    import torch
+    rows = cfg.T * cfg.k
+    shapes = [("gate_up", rows, cfg.d, 2 * cfg.f), ("down", rows, cfg.f, cfg.d), ("dx", rows, 2 * cfg.f, cfg.d)]
+    out = {}
+    for name, M, K, N in shapes:
+        a = torch.randn(M, K, device="cuda", dtype=torch.bfloat16)
+        b = torch.randn(N, K, device="cuda", dtype=torch.bfloat16)
+        for _ in range(3):
+            a @ b.t()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            a @ b.t()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / steps
+        tf = 2.0 * M * K * N / us / 1e6
+        out[name] = {"M": M, "K": K, "N": N, "us": round(us, 1), "TFLOP/s": round(tf, 1),
+                     "frac": round(tf / BF16_PEAK_TFLOPS, 4)}
+        del a, b
+    return {"dense_reference": "torch.matmul (hipBLASLt), bf16", "workload": cfg.name, "shapes": out}
+
+
 def memory_amortisation(P, parties=(1, 2, 4, 8)):
     """The per-party memory claim of Sec. 3 (experts sharded over n parties): one party's peak device memory for
     the expert layer's training step when it hosts all E experts or E/n of them. The row-space buffers keep their
@@ -298,6 +325,9 @@ def main():
                     help="instead of the benchmark: peak device memory of one party's expert-layer training step "
                          "(fwd, bwd, AdamW update) hosting all 64 experts of the T=8192/d=2048/f=1408/E=64/k=4 "
                          "layer or 1/n of them (n = 2, 4, 8 parties), measured and accounted")
+    ap.add_argument("--dense-reference", action="store_true",
+                    help="instead of the benchmark: the vendor's dense bf16 GEMM (torch.matmul) on the workload's "
+                         "gate|up, down and dX shapes with all routed rows as one matrix (context for the roofline)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="before the warm-up, copy a 256 MiB device buffer three times (the reference kernel "
                          "that scales the HBM byte counters of a rocprofv3 --pmc run)")
@@ -315,6 +345,9 @@ def main():
     P.lib()
     if args.memory:
         print(json.dumps(memory_amortisation(P)), flush=True)
+        return
+    if args.dense_reference:
+        print(json.dumps(dense_reference(pick_workload(args.workload))), flush=True)
         return
     if args.copy_calibration:
         src = torch.ones(COPY_CAL_BYTES // 4, dtype=torch.float32, device="cuda")
