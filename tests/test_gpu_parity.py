@@ -80,6 +80,18 @@ def small_cases():
     C["tail_tiles_forced_counts"] = (LayerConfig("tt", T=2048, d=256, f=2048, E=len(tail_counts), k=2, bias="party",
                                                  parties=2048, seed=26), forced_counts)
 
+    # d_model = 4096 selects the software-pipelined one-wavefront-per-SIMD tile for every contraction but the down
+    # projection: ragged tail m-tiles (about 150 rows per expert, 600 shared-expert rows), a last n-tile of 128
+    # columns (f = 384), weight gradients with an odd number of 32-deep K-tiles, and groups with no rows at all
+    C["pipelined_d4096_ragged_shared"] = (LayerConfig("p4", T=600, d=4096, f=384, E=8, k=2, n_shared=1, seed=32), None)
+
+    def two_empty(inp):
+        inp.logit_bias[0, 1] = -1e4
+        inp.logit_bias[0, 6] = -1e4
+        inp.logit_bias[0, 3] = 3.0  # one heavy expert: several m-tiles
+    C["pipelined_d4096_empty_experts"] = (LayerConfig("p4e", T=512, d=4096, f=256, E=8, k=2, bias="forced_empty",
+                                                      seed=33), two_empty)
+
     def zero_router(inp):
         inp.w_router[:] = 0
     C["ties_all_equal"] = (LayerConfig("z", T=256, d=128, f=128, E=8, k=3, seed=21), zero_router)
