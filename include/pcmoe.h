@@ -29,9 +29,10 @@
  *     MOE_ERR_INVALID_ARGUMENT: null or misaligned pointer, k<1, k>E, bad shard range,
  *       local_count < 1 (a party hosts at least one routed expert), bias_groups not dividing T, bad dtype.
  *     MOE_ERR_UNSUPPORTED: d_model or d_ff not a multiple of 128, E > 256, k > 8,
- *       local_count + n_shared > 511, T*k beyond int32 slot indexing, T * max(d_model, 2*d_ff) * elem_bytes
- *       >= 2^31 (one expert group's widest operand, addressed with 32-bit offsets), or
- *       d_ff * d_model * elem_bytes >= 2^31 (one expert's weight matrix).
+ *       local_count + n_shared > 511, T*k beyond int32 slot indexing, (T + 256) * max(d_model, 2*d_ff) *
+ *       elem_bytes >= 2^31 (one expert group's widest operand and a tile past its end, addressed with 32-bit
+ *       offsets), or (m + 256) * m * elem_bytes >= 2^31 with m = max(d_model, d_ff) (one expert's weight
+ *       matrix and a tile past its end).
  *     MOE_ERR_WORKSPACE_TOO_SMALL: ws_bytes below moe_workspace_size(). MOE_ERR_HIP: a kernel launch failed.
  *   - Calls are reentrant; concurrent calls must use distinct output and workspace buffers.
  *   - Global state: the thread-local error string, and the per-kernel timing state of the measurement

@@ -66,14 +66,18 @@ moe_status check_desc(const moe_desc* d) {
   // The grouped GEMMs address one group's operand rows and one expert's weight matrix through 32-bit buffer
   // ranges and 32-bit lane offsets. A group holds at most T rows (a token selects an expert once; a shared
   // expert takes every token), and its widest row is max(d_model, 2 d_ff) elements (x / dY rows, or the
-  // G|U and dG|dU rows).
+  // G|U and dG|dU rows). A tile's lanes address up to one 256-row tile past the last row of a group (the
+  // rows of a group's last m-tile, the K rows of a weight gradient's last K-tile) or of a weight matrix (the
+  // last n-tile): those offsets, too, stay below 2^31.
   const int64_t es = d->dtype == MOE_BF16 ? 2 : 4;
   const int64_t row_bytes = (int64_t)(d->d_model > 2 * d->d_ff ? d->d_model : 2 * d->d_ff) * es;
-  if ((int64_t)d->T * row_bytes >= ((int64_t)1 << 31))
-    return fail(MOE_ERR_UNSUPPORTED, "T=%d rows of %lld bytes exceed the 2 GiB extent of one operand group", d->T,
-                (long long)row_bytes);
-  if ((int64_t)d->d_ff * d->d_model * es >= ((int64_t)1 << 31))
-    return fail(MOE_ERR_UNSUPPORTED, "one expert's %d x %d weight matrix exceeds 2 GiB", d->d_ff, d->d_model);
+  if (((int64_t)d->T + 256) * row_bytes >= ((int64_t)1 << 31))
+    return fail(MOE_ERR_UNSUPPORTED, "T=%d (+ 256) rows of %lld bytes exceed the 2 GiB extent of one operand group",
+                d->T, (long long)row_bytes);
+  const int64_t wmax = d->d_ff > d->d_model ? d->d_ff : d->d_model;
+  if ((wmax + 256) * wmax * es >= ((int64_t)1 << 31))
+    return fail(MOE_ERR_UNSUPPORTED, "one expert's %d x %d weight matrix (+ 256 rows) exceeds 2 GiB", d->d_ff,
+                d->d_model);
   return MOE_OK;
 }
 

@@ -84,8 +84,8 @@ def test_extent_limits_admit_the_workloads():
     for c in CONFIGS.values():
         d = P.make_desc(c.T, c.d, c.f, c.E, c.k, c.local_begin, c.n_local, c.n_shared, c.renormalize, c.dtype)
         assert P.moe_workspace_size(d, P.MOE_WS_FFN_SAVED) > 0, c.name
-    # largest T for d_ff = 14336 in bf16: T * 2 * 14336 * 2 < 2^31
-    t_max = ((1 << 31) - 1) // (4 * 14336)
+    # largest T for d_ff = 14336 in bf16: (T + 256) * 2 * 14336 * 2 < 2^31
+    t_max = ((1 << 31) - 1) // (4 * 14336) - 256
     ok = desc(T=t_max, d_model=4096, d_ff=14336, n_experts=8, top_k=2, dtype="bf16")
     assert P.moe_workspace_size(ok, P.MOE_WS_FFN_SAVED) > 0
     over = desc(T=t_max + 1, d_model=4096, d_ff=14336, n_experts=8, top_k=2, dtype="bf16")
