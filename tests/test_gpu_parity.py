@@ -6,6 +6,9 @@ benchmark times; the two largest (T=8192 d=4096 f=14336, and T=16384 with 64 exp
 against the oracle evaluated one expert group at a time. Routing indices and the permutation are bit-exact
 everywhere."""
 import dataclasses
+import os
+import subprocess
+import sys
 
 import numpy as np
 import pytest
@@ -116,6 +119,35 @@ def test_layer_small(name):
     layer, _ = run_gpu(cfg, inp)
     errs = check_full(cfg, inp, layer)
     log(f"[parity] {name}: " + " ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+
+
+def run_small_bf16_cases():
+    """Every bf16 small case, in this process (the child of the test below)."""
+    for name, (cfg, edit) in SMALL.items():
+        if cfg.dtype != "bf16":
+            continue
+        inp = make_inputs(cfg, with_dy=True)
+        if edit:
+            edit(inp)
+        layer, _ = run_gpu(cfg, inp)
+        errs = check_full(cfg, inp, layer)
+        log(f"[parity, pipelined tile forced] {name}: max rel err {max(errs.values()):.2e}")
+
+
+@pytest.mark.timeout(400)
+def test_layer_small_pipelined_tile_forced():
+    """The bf16 small cases again with the software-pipelined one-wavefront-per-SIMD tile forced on all six
+    contractions (by default it is chosen only at d_model >= 4096): ragged and empty groups, tails, E = 256 with 511
+    groups, ragged last n-tiles. One child process, because the tile override is read once per process."""
+    here = os.path.dirname(os.path.abspath(__file__))
+    env = dict(os.environ, PCMOE_GEMM_TILES=",".join(f"{k}=256x256w4" for k in range(6)))
+    code = (f"import sys; sys.path.insert(0, {os.path.dirname(here)!r}); sys.path.insert(0, {here!r}); "
+            "import test_gpu_parity as T; T.run_small_bf16_cases()")
+    log("[parity] small bf16 cases with the pipelined tile forced (child process)")
+    r = subprocess.run([sys.executable, "-u", "-c", code], env=env, capture_output=True, text=True, timeout=380)
+    log(r.stdout[-4000:])
+    assert r.returncode == 0, r.stderr[-4000:]
+    assert r.stdout.count("[parity, pipelined tile forced]") == sum(c.dtype == "bf16" for c, _ in SMALL.values())
 
 
 def test_deterministic_bits():
