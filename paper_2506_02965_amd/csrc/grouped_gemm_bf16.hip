@@ -461,7 +461,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
             wait_vmcnt<16>();  // K-tile kt + 1 has landed (kt + 2 and kt + 3 may be in flight)
             barrier();
           }
-          mfma_bf16_agpr(acc[i][j], fa[S][i], fb[S][j]);
+          mfma_bf16_agpr(acc[i][j], fb[S][j], fa[S][i]);  // transposed block: 4 consecutive columns per lane
           if (m >= 16) {
             const int r = m - 16;  // 0..47: a read after every third MFMA, a load after every sixth
             if (r % 3 == 0) {
@@ -519,12 +519,22 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
   constexpr int CPRW = OUT_W / 8;                                  // 16-byte output chunks per row
 #pragma unroll
   for (int part = 0; part < C::FM / FPP; ++part) {
+    if constexpr (C::PIPE) {
+      // The pipelined tile multiplies B by A: lane (q, li) of block (i, j) holds row 16 i + li, columns 16 j + 4 q ..
+      // 16 j + 4 q + 3, staged with one 16-byte write.
 #pragma unroll
-    for (int i = 0; i < FPP; ++i)
+      for (int i = 0; i < FPP; ++i)
 #pragma unroll
-      for (int j = 0; j < C::FN; ++j)
+        for (int j = 0; j < C::FN; ++j)
+          *reinterpret_cast<floatx4*>(st + (16 * i + li) * C::PITCH + 16 * j + 4 * q) = acc[part * FPP + i][j];
+    } else {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) st[(16 * i + 4 * q + r) * C::PITCH + 16 * j + li] = acc[part * FPP + i][j][r];
+      for (int i = 0; i < FPP; ++i)
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) st[(16 * i + 4 * q + r) * C::PITCH + 16 * j + li] = acc[part * FPP + i][j][r];
+    }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's staging writes are done
     __builtin_amdgcn_wave_barrier();
     if constexpr (KIND == BWD_DH) {
