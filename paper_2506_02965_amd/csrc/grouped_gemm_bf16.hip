@@ -617,16 +617,36 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(
 }
 
 // Two independent contractions in one launch: workgroups [0, grid_a) take tiles of KA (the longer
-// K loops, so they start first), the rest tiles of KB. The CUs that KA's tile grid leaves idle
+// K loops, so they start first), the next ones tiles of KB. The CUs that KA's tile grid leaves idle
 // work through KB meanwhile, instead of idling until the next launch.
+// KB's last `dyn` tiles are claimed at run time: each of the `dyn_wg` workgroups from `dyn_first` on takes a
+// ticket (an agent-scope counter that starts at zero) and computes KB tile tiles_b - dyn + ticket, or nothing once
+// the tickets run out. The hardware deals workgroups to the XCDs in turn, whatever their speed; with a share of
+// the tiles left unassigned, the XCDs that run ahead take more of them and all finish together.
 template <int BM, int BN, int BK, int KA, int KB, int STAGES, int WM, int WN>
 __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(
     Cfg2<BM, BN, BK, STAGES, WM, WN>::WAVES_PER_EU))) void gemm_bf16_pair_kernel(GemmArgs pa, GemmArgs pb,
-                                                                                 int grid_a) {
+                                                                                 int grid_a, int dyn_first,
+                                                                                 int dyn, int tiles_b,
+                                                                                 int* tickets) {
   extern __shared__ __align__(16) char smem[];
+  __shared__ int ticket;
   const int bid = blockIdx.x;
-  if (bid < grid_a) gemm_tile<BM, BN, BK, KA, STAGES, WM, WN>(pa, bid, smem);
-  else gemm_tile<BM, BN, BK, KB, STAGES, WM, WN>(pb, bid - grid_a, smem);
+  if (bid < grid_a) {
+    gemm_tile<BM, BN, BK, KA, STAGES, WM, WN>(pa, bid, smem);
+  } else if (bid < dyn_first) {
+    gemm_tile<BM, BN, BK, KB, STAGES, WM, WN>(pb, bid - grid_a, smem);
+  } else {
+    if (threadIdx.x == 0) ticket = __hip_atomic_fetch_add(tickets, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    const int t = ticket;
+    if (t < dyn) gemm_tile<BM, BN, BK, KB, STAGES, WM, WN>(pb, tiles_b - dyn + t, smem);
+  }
+}
+
+// Zeroes the tickets of the paired launches that follow on the stream.
+__global__ void zero_tickets_kernel(int* p, int n) {
+  if ((int)threadIdx.x < n) p[threadIdx.x] = 0;
 }
 
 // ------------------------------------------------------------------------- host side
@@ -662,8 +682,8 @@ static const char* kKindName[6] = {"gemm_fwd_gate_up", "gemm_fwd_down", "gemm_bw
                                    "gemm_wgrad_down", "gemm_wgrad_gate_up"};
 
 template <int BM, int BN, int BK, int KA, int KB, int STAGES, int WM, int WN>
-static hipError_t run_pair2(const GemmArgs& a, long tiles_a, const GemmArgs& b, long tiles_b, hipStream_t s,
-                            const char* name) {
+static hipError_t run_pair2(const GemmArgs& a, long tiles_a, const GemmArgs& b, long tiles_b, int* tickets,
+                            hipStream_t s, const char* name) {
   using C = Cfg2<BM, BN, BK, STAGES, WM, WN>;
   static_assert(C::LDS <= 160 * 1024, "LDS budget of one CU");
   auto kern = gemm_bf16_pair_kernel<BM, BN, BK, KA, KB, STAGES, WM, WN>;
@@ -671,10 +691,14 @@ static hipError_t run_pair2(const GemmArgs& a, long tiles_a, const GemmArgs& b, 
   if (hipError_t e = lds_limit_once((const void*)kern, C::LDS, lds_set); e != hipSuccess) return e;
   // grid_a a multiple of 8 keeps each workgroup of the second contraction on the XCD its index implies
   const int grid_a = (int)((tiles_a + 7) / 8 * 8);
-  const int grid = grid_a + (int)tiles_b;
+  // KB's last eighth of tiles (a multiple of 8) goes to ticket-taking workgroups, 32 more per XCD than tiles
+  const int dyn = tickets ? (int)(tiles_b / 64 * 8) : 0;
+  const int dyn_wg = dyn > 0 ? dyn + 256 : 0;
+  const int dyn_first = grid_a + (int)tiles_b - dyn;
+  const int grid = dyn_first + dyn_wg;
   if (grid <= 0) return hipSuccess;
   KernelTimer kt(name, s);
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(C::NT), C::LDS, s, a, b, grid_a);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(C::NT), C::LDS, s, a, b, grid_a, dyn_first, dyn, (int)tiles_b, tickets);
   return hipGetLastError();
 }
 
@@ -752,9 +776,10 @@ static size_t saved_plan_offset(const moe_desc& d) {
 }
 size_t ffn_saved_bytes(const moe_desc& d) { return saved_plan_offset(d) + plan_bytes(d); }
 size_t ffn_fwd_ws_bytes(const moe_desc&) { return 0; }
+// dG|dU [R, 2f], then the tickets of the two paired launches (bf16)
 size_t ffn_bwd_ws_bytes(const moe_desc& d) {
   const size_t R = (size_t)rows_total(d), es = elem_bytes(d);
-  return align256(R * 2 * d.d_ff * es);
+  return align256(R * 2 * d.d_ff * es) + 256;
 }
 
 struct Plan {
@@ -872,6 +897,15 @@ static hipError_t run(const Prep& p, hipStream_t s) {
   return run_shape<KIND>(p.sh, p.a, p.tiles, s);
 }
 
+// PCMOE_DYN=0 keeps every tile of the paired launches on the workgroup its index implies.
+static bool dynamic_tiles() {
+  static const bool on = [] {
+    const char* env = getenv("PCMOE_DYN");
+    return !(env && env[0] == '0');
+  }();
+  return on;
+}
+
 // PCMOE_PAIR=0 launches the paired contractions one after the other instead.
 static bool pair_enabled() {
   static const bool on = [] {
@@ -884,12 +918,15 @@ static bool pair_enabled() {
 // Independent contractions A and B (no operand of one is written by the other) in one launch when
 // they share a tile shape; A's workgroups come first.
 template <int KA, int KB>
-static hipError_t run_pair(const Prep& A, const Prep& B, hipStream_t s, const char* name) {
+static hipError_t run_pair(const Prep& A, const Prep& B, int* tickets, hipStream_t s, const char* name) {
   if (A.sh == B.sh && pair_enabled()) {
     switch (A.sh) {
-      case T256x256w16: return run_pair2<256, 256, 64, KA, KB, 2, 4, 4>(A.a, A.tiles, B.a, B.tiles, s, name);
-      case T256x256w4: return run_pair2<256, 256, 32, KA, KB, 4, 2, 2>(A.a, A.tiles, B.a, B.tiles, s, name);
-      case T128x128s2: return run_pair2<128, 128, 64, KA, KB, 2, 2, 2>(A.a, A.tiles, B.a, B.tiles, s, name);
+      case T256x256w16:
+        return run_pair2<256, 256, 64, KA, KB, 2, 4, 4>(A.a, A.tiles, B.a, B.tiles, tickets, s, name);
+      case T256x256w4:
+        return run_pair2<256, 256, 32, KA, KB, 4, 2, 2>(A.a, A.tiles, B.a, B.tiles, tickets, s, name);
+      case T128x128s2:
+        return run_pair2<128, 128, 64, KA, KB, 2, 2, 2>(A.a, A.tiles, B.a, B.tiles, tickets, s, name);
       default: break;
     }
   }
@@ -934,13 +971,18 @@ hipError_t launch_ffn_bwd(const moe_desc& d, const void* x, const void* xp, cons
   a_wgu.out = dwg;
   a_wgu.out2 = dwu;
   a_dx.out = dxp;
+  int* tickets = (int*)((char*)ws + align256(R * 2 * d.d_ff * es));
+  if (dynamic_tiles()) {
+    hipLaunchKernelGGL(zero_tickets_kernel, dim3(1), dim3(64), 0, s, tickets, 2);
+    if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+  }
   hipError_t e = run_pair<BWD_DH, WG_DOWN>(prep_ragged<BWD_DH>(d, a, pl, d.d_ff),
-                                           prep_wgrad<WG_DOWN>(d, a_wd, pl, d.d_model, d.d_ff), s,
-                                           "gemm_bwd_dh+wgrad_down");
+                                           prep_wgrad<WG_DOWN>(d, a_wd, pl, d.d_model, d.d_ff),
+                                           dynamic_tiles() ? tickets : nullptr, s, "gemm_bwd_dh+wgrad_down");
   if (e != hipSuccess) return e;
   return run_pair<BWD_DX, WG_GU>(prep_ragged<BWD_DX>(d, a_dx, pl, d.d_model, pair_enabled()),
-                                 prep_wgrad<WG_GU>(d, a_wgu, pl, 2 * d.d_ff, d.d_model), s,
-                                 "gemm_bwd_dx+wgrad_gate_up");
+                                 prep_wgrad<WG_GU>(d, a_wgu, pl, 2 * d.d_ff, d.d_model),
+                                 dynamic_tiles() ? tickets + 1 : nullptr, s, "gemm_bwd_dx+wgrad_gate_up");
 }
 
 }  // namespace pcmoe
