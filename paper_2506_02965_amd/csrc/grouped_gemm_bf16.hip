@@ -517,6 +517,46 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
   constexpr int FPP = C::PART_ROWS / 16;  // fm blocks per part
   constexpr int OUT_W = (KIND == FWD_GU) ? C::WTN / 2 : C::WTN;  // output columns of the wave
   constexpr int CPRW = OUT_W / 8;                                  // 16-byte output chunks per row
+  if constexpr (C::PIPE && (KIND == BWD_DX || KIND == WG_DOWN || KIND == WG_GU)) {
+    // Plain stores of the pipelined tile: each lane rounds its four consecutive columns of a block to bf16 (the
+    // rounding the fp32 staging would apply on the way out) and stages them with one 8-byte write; the 16-byte
+    // output chunks are then read whole. Rows of 128 + 8 bf16 keep both sides free of bank conflicts.
+    constexpr int P16 = C::WTN + 8;
+    char* sb = smem + wave * C::WAVE_EPI;
+#pragma unroll
+    for (int part = 0; part < C::FM / FPP; ++part) {
+#pragma unroll
+      for (int i = 0; i < FPP; ++i)
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j) {
+          const floatx4 v = acc[part * FPP + i][j];
+          uint2 pk;
+          pk.x = pack_bf16x2(v[0], v[1]);
+          pk.y = pack_bf16x2(v[2], v[3]);
+          *reinterpret_cast<uint2*>(sb + ((16 * i + li) * P16 + 16 * j + 4 * q) * 2) = pk;
+        }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's staging writes are done
+      __builtin_amdgcn_wave_barrier();
+      for (int qq = lane; qq < C::PART_ROWS * CPRW; qq += 64) {
+        const int rr = qq / CPRW, cc = (qq % CPRW) * 8;
+        const int m = m0 + wm * C::WTM + part * C::PART_ROWS + rr;
+        if (KT::ragged_m && m >= rows) continue;
+        const Chunk v = *reinterpret_cast<const Chunk*>(sb + (rr * P16 + cc) * 2);
+        if (KIND == BWD_DX) {
+          st_chunk((char*)p.out + ((rs + m) * d + n0 + wn * OUT_W + cc) * ES, v);
+        } else if (KIND == WG_DOWN) {
+          st_chunk((char*)p.out + (((size_t)g * d + m) * f + n0 + wn * OUT_W + cc) * ES, v);
+        } else {  // WG_GU
+          const int col = n0 + wn * OUT_W + cc;
+          char* o = (m < f) ? (char*)p.out + (((size_t)g * f + m) * d + col) * ES
+                            : (char*)p.out2 + (((size_t)g * f + (m - f)) * d + col) * ES;
+          st_chunk(o, v);
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+    return;
+  }
 #pragma unroll
   for (int part = 0; part < C::FM / FPP; ++part) {
     if constexpr (C::PIPE) {
