@@ -20,6 +20,7 @@
 //     contractions of the backward share one launch (gemm_bf16_pair_kernel).
 #include "grouped_gemm.h"
 
+#include <algorithm>
 #include <cstdlib>
 #include <cstring>
 
@@ -721,6 +722,16 @@ static const char* kShapeName[N_SHAPES] = {"128x128s2", "256x128w8", "128x256w8"
 static const char* kKindName[6] = {"gemm_fwd_gate_up", "gemm_fwd_down", "gemm_bwd_dh", "gemm_bwd_dx",
                                    "gemm_wgrad_down", "gemm_wgrad_gate_up"};
 
+static int device_cus();
+// Ticket-claimed tiles in the paired launches (see gemm_bf16_pair_kernel): 1 by default, PCMOE_DYN=0 keeps every tile
+// on the workgroup its index implies, PCMOE_DYN=2 claims some tiles by ticket at any size.
+static int dynamic_tiles() {
+  static const int mode = [] {
+    const char* env = getenv("PCMOE_DYN");
+    return env && (env[0] == '0' || env[0] == '2') ? env[0] - '0' : 1;
+  }();
+  return mode;
+}
 template <int BM, int BN, int BK, int KA, int KB, int STAGES, int WM, int WN>
 static hipError_t run_pair2(const GemmArgs& a, long tiles_a, const GemmArgs& b, long tiles_b, int* tickets,
                             hipStream_t s, const char* name) {
@@ -731,8 +742,12 @@ static hipError_t run_pair2(const GemmArgs& a, long tiles_a, const GemmArgs& b, 
   if (hipError_t e = lds_limit_once((const void*)kern, C::LDS, lds_set); e != hipSuccess) return e;
   // grid_a a multiple of 8 keeps each workgroup of the second contraction on the XCD its index implies
   const int grid_a = (int)((tiles_a + 7) / 8 * 8);
-  // KB's last eighth of tiles (a multiple of 8) goes to ticket-taking workgroups, 32 more per XCD than tiles
-  const int dyn = tickets ? (int)(tiles_b / 64 * 8) : 0;
+  // KB's last eighth of tiles (a multiple of 8) goes to ticket-taking workgroups, 32 more per XCD than tiles, when
+  // KB fills at least 8 rounds of the chip (the extra workgroups cost a few microseconds at the launch's end);
+  // PCMOE_DYN=2 takes at least 8 tiles (all of them below 8) this way at any size
+  int dyn = 0;
+  if (tickets && dynamic_tiles() == 2) dyn = (int)std::min<long>(tiles_b, std::max<long>(tiles_b / 64 * 8, 8));
+  else if (tickets && tiles_b >= 8L * device_cus()) dyn = (int)(tiles_b / 64 * 8);
   const int dyn_wg = dyn > 0 ? dyn + 256 : 0;
   const int dyn_first = grid_a + (int)tiles_b - dyn;
   const int grid = dyn_first + dyn_wg;
@@ -765,7 +780,6 @@ static hipError_t run_shape(int shape, const GemmArgs& a, long tiles, hipStream_
 // Default shape per contraction; PCMOE_GEMM_TILES="<kind>=<shape>,..." overrides (kind 0..5 as in
 // GemmKind, shape as in kShapeName), e.g. "0=256x256s2,5=128x256s3".
 static long mtile_bound2(const moe_desc& d, int bm);
-static int device_cus();
 static int tile_shape(int kind, const moe_desc& d) {
   struct Overrides {  // parsed once (thread-safe static initialisation)
     int table[6] = {-1, -1, -1, -1, -1, -1};
@@ -937,14 +951,6 @@ static hipError_t run(const Prep& p, hipStream_t s) {
   return run_shape<KIND>(p.sh, p.a, p.tiles, s);
 }
 
-// PCMOE_DYN=0 keeps every tile of the paired launches on the workgroup its index implies.
-static bool dynamic_tiles() {
-  static const bool on = [] {
-    const char* env = getenv("PCMOE_DYN");
-    return !(env && env[0] == '0');
-  }();
-  return on;
-}
 
 // PCMOE_PAIR=0 launches the paired contractions one after the other instead.
 static bool pair_enabled() {

@@ -121,8 +121,8 @@ def test_layer_small(name):
     log(f"[parity] {name}: " + " ".join(f"{k}={v:.2e}" for k, v in errs.items()))
 
 
-def run_small_bf16_cases():
-    """Every bf16 small case, in this process (the child of the test below)."""
+def run_small_bf16_cases(tag):
+    """Every bf16 small case, in this process (the child of the tests below)."""
     for name, (cfg, edit) in SMALL.items():
         if cfg.dtype != "bf16":
             continue
@@ -131,23 +131,37 @@ def run_small_bf16_cases():
             edit(inp)
         layer, _ = run_gpu(cfg, inp)
         errs = check_full(cfg, inp, layer)
-        log(f"[parity, pipelined tile forced] {name}: max rel err {max(errs.values()):.2e}")
+        log(f"[parity, {tag}] {name}: max rel err {max(errs.values()):.2e}")
+
+
+def run_small_in_child(tag, **env_over):
+    """The bf16 small cases in one child process with environment overrides (read once per process)."""
+    here = os.path.dirname(os.path.abspath(__file__))
+    env = dict(os.environ, **env_over)
+    code = (f"import sys; sys.path.insert(0, {os.path.dirname(here)!r}); sys.path.insert(0, {here!r}); "
+            f"import test_gpu_parity as T; T.run_small_bf16_cases({tag!r})")
+    log(f"[parity] small bf16 cases, {tag} (child process)")
+    r = subprocess.run([sys.executable, "-u", "-c", code], env=env, capture_output=True, text=True, timeout=380)
+    log(r.stdout[-4000:])
+    assert r.returncode == 0, r.stderr[-4000:]
+    assert r.stdout.count(f"[parity, {tag}]") == sum(c.dtype == "bf16" for c, _ in SMALL.values())
 
 
 @pytest.mark.timeout(400)
 def test_layer_small_pipelined_tile_forced():
     """The bf16 small cases again with the software-pipelined one-wavefront-per-SIMD tile forced on all six
     contractions (by default it is chosen only at d_model >= 4096): ragged and empty groups, tails, E = 256 with 511
-    groups, ragged last n-tiles. One child process, because the tile override is read once per process."""
-    here = os.path.dirname(os.path.abspath(__file__))
-    env = dict(os.environ, PCMOE_GEMM_TILES=",".join(f"{k}=256x256w4" for k in range(6)))
-    code = (f"import sys; sys.path.insert(0, {os.path.dirname(here)!r}); sys.path.insert(0, {here!r}); "
-            "import test_gpu_parity as T; T.run_small_bf16_cases()")
-    log("[parity] small bf16 cases with the pipelined tile forced (child process)")
-    r = subprocess.run([sys.executable, "-u", "-c", code], env=env, capture_output=True, text=True, timeout=380)
-    log(r.stdout[-4000:])
-    assert r.returncode == 0, r.stderr[-4000:]
-    assert r.stdout.count("[parity, pipelined tile forced]") == sum(c.dtype == "bf16" for c, _ in SMALL.values())
+    groups, ragged last n-tiles; the paired launches also claim their last weight-gradient tiles by ticket (by
+    default only when those fill 8 rounds of the chip)."""
+    run_small_in_child("pipelined tile forced", PCMOE_GEMM_TILES=",".join(f"{k}=256x256w4" for k in range(6)),
+                       PCMOE_DYN="2")
+
+
+@pytest.mark.timeout(400)
+def test_layer_small_ticket_tiles_forced():
+    """The bf16 small cases with the default tiles and ticket-claimed weight-gradient tiles in every paired launch,
+    down to groups with a single tile."""
+    run_small_in_child("ticket tiles forced", PCMOE_DYN="2")
 
 
 def test_deterministic_bits():
