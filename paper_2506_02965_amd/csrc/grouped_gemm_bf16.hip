@@ -546,12 +546,12 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
         if (KIND == BWD_DX) {
           st_chunk((char*)p.out + ((rs + m) * d + n0 + wn * OUT_W + cc) * ES, v);
         } else if (KIND == WG_DOWN) {
-          st_chunk((char*)p.out + (((size_t)g * d + m) * f + n0 + wn * OUT_W + cc) * ES, v);
+          st_chunk_nt((char*)p.out + (((size_t)g * d + m) * f + n0 + wn * OUT_W + cc) * ES, v);
         } else {  // WG_GU
           const int col = n0 + wn * OUT_W + cc;
           char* o = (m < f) ? (char*)p.out + (((size_t)g * f + m) * d + col) * ES
                             : (char*)p.out2 + (((size_t)g * f + (m - f)) * d + col) * ES;
-          st_chunk(o, v);
+          st_chunk_nt(o, v);
         }
       }
       __builtin_amdgcn_wave_barrier();
@@ -638,12 +638,12 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
       } else if (KIND == FWD_DOWN || KIND == BWD_DX) {
         st_chunk((char*)p.out + ((rs + m) * d + n0 + wn * OUT_W + cc) * ES, f_to_chunk<bf16>(v));
       } else if (KIND == WG_DOWN) {
-        st_chunk((char*)p.out + (((size_t)g * d + m) * f + n0 + wn * OUT_W + cc) * ES, f_to_chunk<bf16>(v));
+        st_chunk_nt((char*)p.out + (((size_t)g * d + m) * f + n0 + wn * OUT_W + cc) * ES, f_to_chunk<bf16>(v));
       } else {  // WG_GU
         const int col = n0 + wn * OUT_W + cc;
         char* o = (m < f) ? (char*)p.out + (((size_t)g * f + m) * d + col) * ES
                           : (char*)p.out2 + (((size_t)g * f + (m - f)) * d + col) * ES;
-        st_chunk(o, f_to_chunk<bf16>(v));
+        st_chunk_nt(o, f_to_chunk<bf16>(v));
       }
     }
     __builtin_amdgcn_wave_barrier();

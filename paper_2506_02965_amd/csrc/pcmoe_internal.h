@@ -70,6 +70,13 @@ template <> __device__ __forceinline__ Chunk f_to_chunk<bf16>(const float* in) {
 
 __device__ __forceinline__ Chunk ld_chunk(const void* p) { return *reinterpret_cast<const Chunk*>(p); }
 __device__ __forceinline__ void st_chunk(void* p, const Chunk& c) { *reinterpret_cast<Chunk*>(p) = c; }
+// The same store marked non-temporal: for outputs that no kernel reads soon (weight gradients, the saved G|U), so
+// that they do not push out of the last-level cache what the next kernels read.
+__device__ __forceinline__ void st_chunk_nt(void* p, const Chunk& c) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 v = {c.w[0], c.w[1], c.w[2], c.w[3]};
+  __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+}
 __device__ __forceinline__ Chunk zero_chunk() {
   Chunk c;
   c.w[0] = c.w[1] = c.w[2] = c.w[3] = 0u;
