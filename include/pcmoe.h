@@ -177,7 +177,9 @@ moe_status moe_combine_bwd(const moe_desc* desc, const void* dy, const void* y_p
  *   dx_perm  [R, d] dtype out: input gradient per row (row space)
  *   dw_gate, dw_up [local_count + n_shared, f, d] dtype out; dw_down [.., d, f] dtype out.
  *            Hosted experts that received no row get exact zeros.
- *   ws       MOE_WS_FFN_BWD bytes of scratch
+ *   ws       MOE_WS_FFN_BWD bytes of scratch: dG|dU, and two tile counters that the call zeroes before its
+ *            GEMM launches claim their last weight-gradient tiles from them. Calls that overlap on the
+ *            GPU need workspaces of their own.
  */
 moe_status moe_expert_ffn_bwd(const moe_desc* desc, const void* x, const void* x_perm, const void* dy,
                               const void* dy_perm, const int32_t* offsets, const void* w_gate, const void* w_up,
