@@ -29,6 +29,7 @@ struct GemmArgs {
   void* out2;                 // dW_up (WG_GU)
   int wg_interleave;          // weight gradients: with near-equal groups (order[G] = 1), tile L belongs to group
                               // order[L % G] (round-robin over groups)
+  int* tickets;               // single-contraction bf16 launches: a zeroed counter for ticket-claimed tiles, or null
 };
 
 template <int KIND> struct KindTraits;

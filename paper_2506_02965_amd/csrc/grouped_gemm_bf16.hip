@@ -652,9 +652,18 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
 
 template <int BM, int BN, int BK, int KIND, int STAGES, int WM, int WN>
 __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(
-    Cfg2<BM, BN, BK, STAGES, WM, WN>::WAVES_PER_EU))) void gemm_bf16_kernel(GemmArgs p) {
+    Cfg2<BM, BN, BK, STAGES, WM, WN>::WAVES_PER_EU))) void gemm_bf16_kernel(GemmArgs p, int dyn_first, int dyn) {
   extern __shared__ __align__(16) char smem[];
-  gemm_tile<BM, BN, BK, KIND, STAGES, WM, WN>(p, blockIdx.x, smem);
+  __shared__ int ticket;
+  const int bid = blockIdx.x;
+  if (bid < dyn_first) {
+    gemm_tile<BM, BN, BK, KIND, STAGES, WM, WN>(p, bid, smem);
+  } else {  // ticket-claimed: workgroup index dyn_first + ticket of the static grid (see gemm_bf16_pair_kernel)
+    if (threadIdx.x == 0) ticket = __hip_atomic_fetch_add(p.tickets, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    const int t = ticket;
+    if (t < dyn) gemm_tile<BM, BN, BK, KIND, STAGES, WM, WN>(p, dyn_first + t, smem);
+  }
 }
 
 // Two independent contractions in one launch: workgroups [0, grid_a) take tiles of KA (the longer
@@ -692,6 +701,16 @@ __global__ void zero_tickets_kernel(int* p, int n) {
 
 // ------------------------------------------------------------------------- host side
 
+static int device_cus();
+// Ticket-claimed tiles (see gemm_bf16_pair_kernel): 1 by default, PCMOE_DYN=0 keeps every tile on the workgroup its
+// index implies, PCMOE_DYN=2 claims some tiles by ticket at any size.
+static int dynamic_tiles() {
+  static const int mode = [] {
+    const char* env = getenv("PCMOE_DYN");
+    return env && (env[0] == '0' || env[0] == '2') ? env[0] - '0' : 1;
+  }();
+  return mode;
+}
 template <int BM, int BN, int BK, int KIND, int STAGES, int WM, int WN>
 static hipError_t run2(const GemmArgs& a, long tiles, hipStream_t s, const char* name) {
   using C = Cfg2<BM, BN, BK, STAGES, WM, WN>;
@@ -701,8 +720,13 @@ static hipError_t run2(const GemmArgs& a, long tiles, hipStream_t s, const char*
   if (hipError_t e = lds_limit_once((const void*)kern, C::LDS, lds_set); e != hipSuccess) return e;
   const int grid = (int)((tiles + 7) / 8 * 8);
   if (grid <= 0) return hipSuccess;
+  // with a.tickets, the last eighth of the grid's workgroup indices is claimed by ticket (as in the paired launches)
+  int dyn = 0;
+  if (a.tickets && dynamic_tiles() == 2) dyn = std::min(grid, std::max(grid / 64 * 8, 8));
+  else if (a.tickets && grid >= 8 * device_cus()) dyn = grid / 64 * 8;
+  const int dyn_first = grid - dyn, dyn_wg = dyn > 0 ? dyn + 256 : 0;
   KernelTimer kt(name, s);
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(C::NT), C::LDS, s, a);
+  hipLaunchKernelGGL(kern, dim3(dyn_first + dyn_wg), dim3(C::NT), C::LDS, s, a, dyn_first, dyn);
   return hipGetLastError();
 }
 
@@ -722,16 +746,6 @@ static const char* kShapeName[N_SHAPES] = {"128x128s2", "256x128w8", "128x256w8"
 static const char* kKindName[6] = {"gemm_fwd_gate_up", "gemm_fwd_down", "gemm_bwd_dh", "gemm_bwd_dx",
                                    "gemm_wgrad_down", "gemm_wgrad_gate_up"};
 
-static int device_cus();
-// Ticket-claimed tiles in the paired launches (see gemm_bf16_pair_kernel): 1 by default, PCMOE_DYN=0 keeps every tile
-// on the workgroup its index implies, PCMOE_DYN=2 claims some tiles by ticket at any size.
-static int dynamic_tiles() {
-  static const int mode = [] {
-    const char* env = getenv("PCMOE_DYN");
-    return env && (env[0] == '0' || env[0] == '2') ? env[0] - '0' : 1;
-  }();
-  return mode;
-}
 template <int BM, int BN, int BK, int KA, int KB, int STAGES, int WM, int WN>
 static hipError_t run_pair2(const GemmArgs& a, long tiles_a, const GemmArgs& b, long tiles_b, int* tickets,
                             hipStream_t s, const char* name) {
@@ -828,7 +842,8 @@ static size_t saved_plan_offset(const moe_desc& d) {
   const size_t R = (size_t)rows_total(d), es = elem_bytes(d);
   return align256(R * 2 * d.d_ff * es) + align256(R * d.d_ff * es);
 }
-size_t ffn_saved_bytes(const moe_desc& d) { return saved_plan_offset(d) + plan_bytes(d); }
+// ... and 256 bytes for the forward's tile tickets
+size_t ffn_saved_bytes(const moe_desc& d) { return saved_plan_offset(d) + align256(plan_bytes(d)) + 256; }
 size_t ffn_fwd_ws_bytes(const moe_desc&) { return 0; }
 // dG|dU [R, 2f], then the tickets of the two paired launches (bf16)
 size_t ffn_bwd_ws_bytes(const moe_desc& d) {
@@ -992,7 +1007,13 @@ hipError_t launch_ffn_fwd(const moe_desc& d, const void* x, const void* xp, cons
   a.h = (char*)saved + align256(R * 2 * d.d_ff * 2);
   a.out = yp;
   hipError_t e;
-  if ((e = run<FWD_GU>(prep_ragged<FWD_GU>(d, a, pl, 2 * d.d_ff), s)) != hipSuccess) return e;
+  GemmArgs a_gu = a;
+  if (dynamic_tiles()) {
+    a_gu.tickets = (int*)((char*)saved + saved_plan_offset(d) + align256(plan_bytes(d)));
+    hipLaunchKernelGGL(zero_tickets_kernel, dim3(1), dim3(64), 0, s, a_gu.tickets, 1);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  if ((e = run<FWD_GU>(prep_ragged<FWD_GU>(d, a_gu, pl, 2 * d.d_ff), s)) != hipSuccess) return e;
   return run<FWD_DOWN>(prep_ragged<FWD_DOWN>(d, a, pl, d.d_model), s);
 }
 
