@@ -842,7 +842,7 @@ static size_t saved_plan_offset(const moe_desc& d) {
   const size_t R = (size_t)rows_total(d), es = elem_bytes(d);
   return align256(R * 2 * d.d_ff * es) + align256(R * d.d_ff * es);
 }
-// ... and 256 bytes for the forward's tile tickets
+// ... and 256 bytes for the forward launches' tile tickets
 size_t ffn_saved_bytes(const moe_desc& d) { return saved_plan_offset(d) + align256(plan_bytes(d)) + 256; }
 size_t ffn_fwd_ws_bytes(const moe_desc&) { return 0; }
 // dG|dU [R, 2f], then the tickets of the two paired launches (bf16)
@@ -1007,14 +1007,15 @@ hipError_t launch_ffn_fwd(const moe_desc& d, const void* x, const void* xp, cons
   a.h = (char*)saved + align256(R * 2 * d.d_ff * 2);
   a.out = yp;
   hipError_t e;
-  GemmArgs a_gu = a;
+  GemmArgs a_gu = a, a_down = a;
   if (dynamic_tiles()) {
     a_gu.tickets = (int*)((char*)saved + saved_plan_offset(d) + align256(plan_bytes(d)));
-    hipLaunchKernelGGL(zero_tickets_kernel, dim3(1), dim3(64), 0, s, a_gu.tickets, 1);
+    a_down.tickets = a_gu.tickets + 1;
+    hipLaunchKernelGGL(zero_tickets_kernel, dim3(1), dim3(64), 0, s, a_gu.tickets, 2);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if ((e = run<FWD_GU>(prep_ragged<FWD_GU>(d, a_gu, pl, 2 * d.d_ff), s)) != hipSuccess) return e;
-  return run<FWD_DOWN>(prep_ragged<FWD_DOWN>(d, a, pl, d.d_model), s);
+  return run<FWD_DOWN>(prep_ragged<FWD_DOWN>(d, a_down, pl, d.d_model), s);
 }
 
 hipError_t launch_ffn_bwd(const moe_desc& d, const void* x, const void* xp, const void* dy, const void* dyp,
