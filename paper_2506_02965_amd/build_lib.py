@@ -21,8 +21,12 @@ SOURCES = ["api.hip", "router.hip", "permute.hip", "combine.hip", "grouped_gemm_
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # packed fp32 instructions are disabled for every device code object of this library
+# -amdgpu-atomic-optimizer-strategy=None: a single lane's atomic stays a plain atomic whose result is waited for where
+# it is used. The optimizer turns it into a wave-wide scan that waits for the result at once, which would make the
+# tile claims of the persistent weight-gradient loop wait for every operand load issued before them.
 CFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang",
-          "-packed-fp32-ops", "-I", os.path.join(ROOT, "include"), "-Wall", "-Wno-unused-function"]
+          "-packed-fp32-ops", "-mllvm", "-amdgpu-atomic-optimizer-strategy=None", "-I", os.path.join(ROOT, "include"),
+          "-Wall", "-Wno-unused-function"]
 
 
 def _run(cmd, verbose):

@@ -666,6 +666,239 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(
   }
 }
 
+// Weight-gradient tiles of the pipelined 256 x 256 shape in persistent workgroups (one per CU), for the second
+// contraction of a paired launch. Tile L belongs to XCD L mod 8 (the static mapping's L2 locality); each XCD's
+// workgroups take its tiles in order from a counter of their own, and take another XCD's once theirs run out.
+// Per tile, after the K loop: the next tile is decoded, its first four K-tiles are issued into the operand ring, and
+// only then is the finished tile written out, through a staging area past the ring (16-row parts, bf16) that no load
+// touches. The next K loop starts once every load and store has completed (vmcnt(0)), so no wait count ever spans
+// stores. A tile is claimed one tile ahead from the workgroup's own XCD counter (the increment is issued with the
+// prologue loads and its result read after the next K loop); only when that share is exhausted are the other XCDs'
+// counters tried, one after the other. The loop ends when every counter is past its XCD's share, so every
+// wavefront leaves.
+constexpr int WG_STG_ROWS = 16;                              // staging rows per part
+constexpr int WG_STG_WAVE = WG_STG_ROWS * (128 + 8) * 2;         // one wavefront's staging area (bf16)
+constexpr int WG_LDS = Cfg2<256, 256, 32, 4, 2, 2>::LDS_MAIN + 4 * WG_STG_WAVE;
+struct WgTile {
+  int g, m0, n0, rows;
+  size_t rs;
+  bool cols;  // this wavefront's columns lie inside N
+};
+// Tile for claim result t of XCD x's counter, or -1 past x's share (tiles L = x, x + 8, ...).
+__device__ __forceinline__ int wg_tile_of(int t, int x, int n_tiles) {
+  return t >= 0 && t < ((n_tiles - x + 7) >> 3) ? 8 * t + x : -1;
+}
+// The other XCDs' counters in turn (lane 0 of wave 0 only): tile L, or -1 once every share is taken.
+__device__ __forceinline__ int wg_steal(int* queues, int xcc, int n_tiles) {
+  for (int i = 1; i < 8; ++i) {
+    const int x = (xcc + i) & 7;
+    const int L = wg_tile_of(__hip_atomic_fetch_add(queues + x, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), x,
+                             n_tiles);
+    if (L >= 0) return L;
+  }
+  return -1;
+}
+
+template <int KIND>
+__device__ __forceinline__ void wg_persistent(const GemmArgs& p, char* smem, int* queues, int n_tiles) {
+  static_assert(KIND == WG_DOWN || KIND == WG_GU, "weight gradients only");
+  using C = Cfg2<256, 256, 32, 4, 2, 2>;
+  constexpr int ES = 2;
+  constexpr int STG_ROWS = WG_STG_ROWS, P16 = C::WTN + 8, STG_WAVE = WG_STG_WAVE;
+  static_assert(STG_WAVE == STG_ROWS * P16 * 2 && WG_LDS <= 160 * 1024, "ring and staging share the LDS");
+  __shared__ int next_tile;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / 2, wn = wave % 2;
+  const int q = lane >> 4, li = lane & 15;
+  const int d = p.d, f = p.f;
+  const int xcc = (int)(__builtin_amdgcn_s_getreg((3 << 11) | 20) & 7);  // HW_REG_XCC_ID
+  const uint32_t lds_base = lds_addr(smem);
+  char* stg = smem + C::LDS_MAIN + wave * STG_WAVE;
+
+  if (tid == 0) {
+    int L0 = wg_tile_of(__hip_atomic_fetch_add(queues + xcc, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), xcc,
+                        n_tiles);
+    next_tile = L0 >= 0 ? L0 : wg_steal(queues, xcc, n_tiles);
+  }
+  __syncthreads();
+  const int L = next_tile;
+  if (L < 0) return;
+
+  // per-tile operand state
+  int32x4 ra, rb;
+  int a_ld, b_ld, va[4], vb[4], KTN = 0;
+  WgTile cur;
+  const auto setup = [&](int tile, WgTile& w) {
+    TileIdx ti;
+    decode_tile<false>(p, tile, ti);
+    w.g = ti.g;
+    const bool routed = ti.g < p.Eloc;
+    w.rows = ti.rows;
+    w.rs = routed ? (size_t)ti.row0 : (size_t)p.rows_cap + (size_t)(ti.g - p.Eloc) * p.T;
+    w.m0 = ti.mt * 256;
+    w.n0 = ti.nt * 256;
+    w.cols = w.n0 + wn * C::WTN < p.n_extent;
+    const char *a_base, *b_base;
+    if (KIND == WG_DOWN) {
+      a_base = routed ? (const char*)p.dyp + w.rs * d * ES : (const char*)p.dy;
+      a_ld = d * ES;
+      b_base = (const char*)p.h + w.rs * f * ES;
+      b_ld = f * ES;
+    } else {
+      a_base = (const char*)p.dgu + w.rs * 2 * f * ES;
+      a_ld = 2 * f * ES;
+      b_base = routed ? (const char*)p.xp + w.rs * d * ES : (const char*)p.x;
+      b_ld = d * ES;
+    }
+    ra = make_rsrc(a_base, (uint32_t)((size_t)w.rows * a_ld));
+    rb = make_rsrc(b_base, (uint32_t)((size_t)w.rows * b_ld));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int jj = wave + 4 * j;
+      const int kr = 2 * jj + (lane >> 5), c = ((lane & 31) - 8 * (kr & 1)) & 31;
+      va[j] = kr * a_ld + (w.m0 + 8 * c) * ES;
+      vb[j] = kr * b_ld + (w.n0 + 8 * c) * ES;
+    }
+    KTN = (w.rows + 31) / 32;
+  };
+  constexpr int OOR = 0x7fffffff;
+  const auto load_one = [&](int kt, int l) {
+    const bool live = kt < KTN;
+    const int k0 = kt * 32;
+    const uint32_t st = lds_base + (kt & 3) * C::STAGE_BYTES;
+    const int jj = wave + 4 * (l & 3);
+    if (l < 4) dma16(ra, st + jj * 1024 + 32 * jj, live ? va[l & 3] + k0 * a_ld : OOR);
+    else dma16(rb, st + C::A_BYTES + jj * 1024 + 32 * jj, live ? vb[l & 3] + k0 * b_ld : OOR);
+  };
+  const auto issue_all = [&](int kt) {
+#pragma unroll
+    for (int l = 0; l < 8; ++l) load_one(kt, l);
+  };
+  const auto barrier = [] { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
+  // transposed fragment reads of the padded K-major layout (both operands), k order swapped in odd lane groups
+  const int kl1 = 8 * q + 4 * (q & 1) + (li >> 2), kl2 = kl1 + 4 - 8 * (q & 1);
+  const auto mk_lane = [&](int kl, int w) {
+    return mk_row(kl) + 128 * ((w + (kl & 1)) & 3) + 16 * ((li & 3) >> 1) + 8 * (li & 1);
+  };
+  const auto frag = [&](const char* S, int wbase, int i) {
+    const int w = wbase / 64 + i / 4;
+    return lds_tr_pair(S + mk_lane(kl1, w) + 32 * (i % 4), S + mk_lane(kl2, w) + 32 * (i % 4));
+  };
+
+  int claim = 0;  // lane 0 of wave 0: the own-XCD counter's value for the tile after the current one
+  setup(L, cur);
+  issue_all(0);
+  issue_all(1);
+  issue_all(2);
+  issue_all(3);
+  if (tid == 0) claim = __hip_atomic_fetch_add(queues + xcc, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();  // every wave has read next_tile
+  for (;;) {
+    floatx4 acc[8][8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this tile's first loads (and any earlier stores) are done
+    barrier();
+    const int KTN2 = (KTN + 1) & ~1;
+    if (!cur.cols) {
+      for (int kt = 0; kt < KTN2; ++kt) {
+        wait_vmcnt<16>();
+        barrier();
+        issue_all(kt + 4);
+      }
+    } else {
+      Chunk fa[2][8], fb[2][8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) fa[0][i] = frag(smem, wm * C::WTM, i);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) fb[0][j] = frag(smem + C::A_BYTES, wn * C::WTN, j);
+      const auto step = [&](int kt, auto set) {
+        constexpr int S = decltype(set)::value;
+        const char* As = smem + ((kt + 1) & 3) * C::STAGE_BYTES;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const int m = i * 8 + j;
+            if (m == 16) {
+              wait_vmcnt<16>();  // K-tile kt + 1 has landed
+              barrier();
+            }
+            mfma_bf16_agpr(acc[i][j], fb[S][j], fa[S][i]);
+            if (m >= 16) {
+              const int r = m - 16;
+              if (r % 3 == 0) {
+                const int t = r / 3;
+                if (t == 0) fa[S ^ 1][0] = frag(As, wm * C::WTM, 0);
+                else if (t <= 8) fb[S ^ 1][t - 1] = frag(As + C::A_BYTES, wn * C::WTN, t - 1);
+                else fa[S ^ 1][t - 8] = frag(As, wm * C::WTM, t - 8);
+              }
+              if (r % 6 == 2) load_one(kt + 4, r / 6);
+            }
+          }
+        }
+      };
+      for (int kt = 0; kt < KTN2; kt += 2) {
+        step(kt, std::integral_constant<int, 0>{});
+        step(kt + 1, std::integral_constant<int, 1>{});
+      }
+    }
+    wait_vmcnt<0>();  // the zero-filling loads past the last K-tile have landed
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+    if (tid == 0) {
+      const int Lc = wg_tile_of(claim, xcc, n_tiles);
+      next_tile = Lc >= 0 ? Lc : wg_steal(queues, xcc, n_tiles);
+    }
+    __syncthreads();  // every wave is done with the ring; next_tile is visible
+    const int Ln = next_tile;
+    const WgTile done = cur;
+    if (Ln >= 0) {
+      setup(Ln, cur);
+      issue_all(0);
+      issue_all(1);
+      issue_all(2);
+      issue_all(3);
+      if (tid == 0) claim = __hip_atomic_fetch_add(queues + xcc, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    // the finished tile, through this wave's staging area past the ring
+    if (done.cols) {
+      constexpr int CPRW = C::WTN / 8;
+#pragma unroll
+      for (int part = 0; part < 8; ++part) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const floatx4 v = acc[part][j];
+          uint2 pk;
+          pk.x = pack_bf16x2(v[0], v[1]);
+          pk.y = pack_bf16x2(v[2], v[3]);
+          *reinterpret_cast<uint2*>(stg + (li * P16 + 16 * j + 4 * q) * 2) = pk;
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int it = 0; it < STG_ROWS * CPRW / 64; ++it) {
+          const int qq = lane + 64 * it, rr = qq / CPRW, cc = (qq % CPRW) * 8;
+          const int m = done.m0 + wm * C::WTM + part * STG_ROWS + rr;
+          const Chunk v = *reinterpret_cast<const Chunk*>(stg + (rr * P16 + cc) * 2);
+          const int col = done.n0 + wn * C::WTN + cc;
+          if (KIND == WG_DOWN) {
+            st_chunk_nt((char*)p.out + (((size_t)done.g * d + m) * f + col) * ES, v);
+          } else {
+            char* o = (m < f) ? (char*)p.out + (((size_t)done.g * f + m) * d + col) * ES
+                              : (char*)p.out2 + (((size_t)done.g * f + (m - f)) * d + col) * ES;
+            st_chunk_nt(o, v);
+          }
+        }
+        __builtin_amdgcn_wave_barrier();
+      }
+    }
+    if (Ln < 0) return;
+  }
+}
+
 // Two independent contractions in one launch: workgroups [0, grid_a) take tiles of KA (the longer
 // K loops, so they start first), the next ones tiles of KB. The CUs that KA's tile grid leaves idle
 // work through KB meanwhile, instead of idling until the next launch.
@@ -684,6 +917,9 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(
   const int bid = blockIdx.x;
   if (bid < grid_a) {
     gemm_tile<BM, BN, BK, KA, STAGES, WM, WN>(pa, bid, smem);
+  } else if (dyn < 0) {  // persistent workgroups for KB (see wg_persistent)
+    if constexpr (Cfg2<BM, BN, BK, STAGES, WM, WN>::PIPE && STAGES == 4 && (KB == WG_DOWN || KB == WG_GU))
+      wg_persistent<KB>(pb, smem, tickets, tiles_b);
   } else if (bid < dyn_first) {
     gemm_tile<BM, BN, BK, KB, STAGES, WM, WN>(pb, bid - grid_a, smem);
   } else {
@@ -746,14 +982,25 @@ static const char* kShapeName[N_SHAPES] = {"128x128s2", "256x128w8", "128x256w8"
 static const char* kKindName[6] = {"gemm_fwd_gate_up", "gemm_fwd_down", "gemm_bwd_dh", "gemm_bwd_dx",
                                    "gemm_wgrad_down", "gemm_wgrad_gate_up"};
 
+// PCMOE_PERSIST=0 keeps the pipelined weight gradients on ticket-claimed tails instead of persistent workgroups.
+static bool persistent_wgrad() {
+  static const bool on = [] {
+    const char* env = getenv("PCMOE_PERSIST");
+    return !(env && env[0] == '0');
+  }();
+  return on;
+}
 template <int BM, int BN, int BK, int KA, int KB, int STAGES, int WM, int WN>
 static hipError_t run_pair2(const GemmArgs& a, long tiles_a, const GemmArgs& b, long tiles_b, int* tickets,
                             hipStream_t s, const char* name) {
   using C = Cfg2<BM, BN, BK, STAGES, WM, WN>;
-  static_assert(C::LDS <= 160 * 1024, "LDS budget of one CU");
+  // the persistent weight-gradient loop stages its epilogue past the operand ring
+  constexpr bool PERSIST = C::PIPE && STAGES == 4 && (KB == WG_DOWN || KB == WG_GU);
+  constexpr int LDS = PERSIST ? (C::LDS > WG_LDS ? C::LDS : WG_LDS) : C::LDS;
+  static_assert(LDS <= 160 * 1024, "LDS budget of one CU");
   auto kern = gemm_bf16_pair_kernel<BM, BN, BK, KA, KB, STAGES, WM, WN>;
   static std::atomic<uint64_t> lds_set{0};
-  if (hipError_t e = lds_limit_once((const void*)kern, C::LDS, lds_set); e != hipSuccess) return e;
+  if (hipError_t e = lds_limit_once((const void*)kern, LDS, lds_set); e != hipSuccess) return e;
   // grid_a a multiple of 8 keeps each workgroup of the second contraction on the XCD its index implies
   const int grid_a = (int)((tiles_a + 7) / 8 * 8);
   // KB's last eighth of tiles (a multiple of 8) goes to ticket-taking workgroups, 32 more per XCD than tiles, when
@@ -762,12 +1009,20 @@ static hipError_t run_pair2(const GemmArgs& a, long tiles_a, const GemmArgs& b, 
   int dyn = 0;
   if (tickets && dynamic_tiles() == 2) dyn = (int)std::min<long>(tiles_b, std::max<long>(tiles_b / 64 * 8, 8));
   else if (tickets && tiles_b >= 8L * device_cus()) dyn = (int)(tiles_b / 64 * 8);
-  const int dyn_wg = dyn > 0 ? dyn + 256 : 0;
-  const int dyn_first = grid_a + (int)tiles_b - dyn;
+  int dyn_wg = dyn > 0 ? dyn + 256 : 0;
+  int dyn_first = grid_a + (int)tiles_b - dyn;
+  // The pipelined tile's weight gradients run in persistent workgroups instead (one per CU; see wg_persistent)
+  if constexpr (PERSIST) {
+    if (dyn > 0 && persistent_wgrad()) {
+      dyn = -1;
+      dyn_first = grid_a;
+      dyn_wg = device_cus();
+    }
+  }
   const int grid = dyn_first + dyn_wg;
   if (grid <= 0) return hipSuccess;
   KernelTimer kt(name, s);
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(C::NT), C::LDS, s, a, b, grid_a, dyn_first, dyn, (int)tiles_b, tickets);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(C::NT), LDS, s, a, b, grid_a, dyn_first, dyn, (int)tiles_b, tickets);
   return hipGetLastError();
 }
 
@@ -1041,7 +1296,7 @@ hipError_t launch_ffn_bwd(const moe_desc& d, const void* x, const void* xp, cons
   a_dx.out = dxp;
   int* tickets = (int*)((char*)ws + align256(R * 2 * d.d_ff * es));
   if (dynamic_tiles()) {
-    hipLaunchKernelGGL(zero_tickets_kernel, dim3(1), dim3(64), 0, s, tickets, 2);
+    hipLaunchKernelGGL(zero_tickets_kernel, dim3(1), dim3(64), 0, s, tickets, 16);
     if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   }
   hipError_t e = run_pair<BWD_DH, WG_DOWN>(prep_ragged<BWD_DH>(d, a, pl, d.d_ff),
@@ -1050,7 +1305,7 @@ hipError_t launch_ffn_bwd(const moe_desc& d, const void* x, const void* xp, cons
   if (e != hipSuccess) return e;
   return run_pair<BWD_DX, WG_GU>(prep_ragged<BWD_DX>(d, a_dx, pl, d.d_model, pair_enabled()),
                                  prep_wgrad<WG_GU>(d, a_wgu, pl, 2 * d.d_ff, d.d_model),
-                                 dynamic_tiles() ? tickets + 1 : nullptr, s, "gemm_bwd_dx+wgrad_gate_up");
+                                 dynamic_tiles() ? tickets + 8 : nullptr, s, "gemm_bwd_dx+wgrad_gate_up");
 }
 
 }  // namespace pcmoe
