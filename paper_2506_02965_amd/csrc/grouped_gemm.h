@@ -60,30 +60,54 @@ struct TileIdx {
   int g, mt, nt;
   int row0, rows;  // the group's first row in its source and its row count
 };
+// The plan arrays a tile decode reads, spread over the wavefront (entry 64 s + lane in slot s).
+struct DecodeArrays {
+  static constexpr int NS = 8;  // 8 x 64 entries per array: groups <= 511
+  int pre[NS], ord[NS], off[NS], tl[NS];
+};
+// One batch of independent loads (a chain of dependent ones costs a memory latency each): the m-tile prefix (ragged
+// kinds), the group order (weight gradients) and the row offsets.
 template <bool RAGGED>
-__device__ __forceinline__ bool decode_tile(const GemmArgs& p, int bid, TileIdx& t) {
-  constexpr int NS = 8;  // 8 x 64 entries per array: groups <= 511
+__device__ __forceinline__ void decode_load(const GemmArgs& p, DecodeArrays& a) {
   const int G = p.Eloc + p.S;
   const int lane = threadIdx.x & 63;
   const int ns = (G + 64) >> 6;  // slots covering entries 0..G
-  // One batch of independent loads (a chain of dependent ones costs a memory latency each): the
-  // m-tile prefix (ragged kinds), the group order (weight gradients) and the row offsets.
-  int pre[NS], ord[NS], off[NS], tl[NS];
   const bool split = RAGGED && p.mt_tail != nullptr;
 #pragma unroll
-  for (int s = 0; s < NS; ++s) {
+  for (int s = 0; s < DecodeArrays::NS; ++s) {
     const int i = 64 * s + lane;
-    pre[s] = 0;
-    ord[s] = 0;
-    off[s] = 0;
-    tl[s] = 0;
+    a.pre[s] = 0;
+    a.ord[s] = 0;
+    a.off[s] = 0;
+    a.tl[s] = 0;
     if (s < ns) {
-      if (RAGGED && i <= G) pre[s] = p.mt_prefix[i];
-      if (split && i <= G) tl[s] = p.mt_tail[i];
-      if (!RAGGED && p.order && i <= G) ord[s] = p.order[i];
-      if (p.Eloc > 0 && i <= p.Eloc) off[s] = p.offsets[i];
+      if (RAGGED && i <= G) a.pre[s] = p.mt_prefix[i];
+      if (split && i <= G) a.tl[s] = p.mt_tail[i];
+      if (!RAGGED && p.order && i <= G) a.ord[s] = p.order[i];
+      if (p.Eloc > 0 && i <= p.Eloc) a.off[s] = p.offsets[i];
     }
   }
+}
+template <bool RAGGED>
+__device__ __forceinline__ bool decode_with(const GemmArgs& p, int bid, const DecodeArrays& a, TileIdx& t);
+template <bool RAGGED>
+__device__ __forceinline__ bool decode_tile(const GemmArgs& p, int bid, TileIdx& t) {
+  DecodeArrays a;
+  decode_load<RAGGED>(p, a);
+  return decode_with<RAGGED>(p, bid, a, t);
+}
+// The decode proper, from arrays loaded by decode_load (a persistent workgroup loads them once).
+template <bool RAGGED>
+__device__ __forceinline__ bool decode_with(const GemmArgs& p, int bid, const DecodeArrays& a, TileIdx& t) {
+  constexpr int NS = DecodeArrays::NS;
+  const int G = p.Eloc + p.S;
+  const int lane = threadIdx.x & 63;
+  const int ns = (G + 64) >> 6;
+  const bool split = RAGGED && p.mt_tail != nullptr;
+  const auto& pre = a.pre;
+  const auto& ord = a.ord;
+  const auto& off = a.off;
+  const auto& tl = a.tl;
   int total;
   if (RAGGED) total = wave_pick(pre, G) * p.n_tiles;
   else total = G * p.m_tiles * p.n_tiles;

@@ -669,7 +669,8 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(
 // Weight-gradient tiles of the pipelined 256 x 256 shape in persistent workgroups (one per CU), for the second
 // contraction of a paired launch. Tile L belongs to XCD L mod 8 (the static mapping's L2 locality); each XCD's
 // workgroups take its tiles in order from a counter of their own, and take another XCD's once theirs run out.
-// Per tile, after the K loop: the next tile is decoded, its first four K-tiles are issued into the operand ring, and
+// Per tile, after the K loop: the next tile is decoded (from plan arrays loaded once, so without a memory round
+// trip), its first four K-tiles are issued into the operand ring, and
 // only then is the finished tile written out, through a staging area past the ring (16-row parts, bf16) that no load
 // touches. The next K loop starts once every load and store has completed (vmcnt(0)), so no wait count ever spans
 // stores. A tile is claimed one tile ahead from the workgroup's own XCD counter (the increment is issued with the
@@ -725,13 +726,16 @@ __device__ __forceinline__ void wg_persistent(const GemmArgs& p, char* smem, int
   const int L = next_tile;
   if (L < 0) return;
 
+  // the plan arrays of the decode, loaded once for every tile of the loop
+  DecodeArrays plan;
+  decode_load<false>(p, plan);
   // per-tile operand state
   int32x4 ra, rb;
   int a_ld, b_ld, va[4], vb[4], KTN = 0;
   WgTile cur;
   const auto setup = [&](int tile, WgTile& w) {
     TileIdx ti;
-    decode_tile<false>(p, tile, ti);
+    decode_with<false>(p, tile, plan, ti);
     w.g = ti.g;
     const bool routed = ti.g < p.Eloc;
     w.rows = ti.rows;
