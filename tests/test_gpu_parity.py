@@ -151,10 +151,18 @@ def run_small_in_child(tag, **env_over):
 def test_layer_small_pipelined_tile_forced():
     """The bf16 small cases again with the software-pipelined one-wavefront-per-SIMD tile forced on all six
     contractions (by default it is chosen only at d_model >= 4096): ragged and empty groups, tails, E = 256 with 511
-    groups, ragged last n-tiles; the paired launches also claim their last weight-gradient tiles by ticket (by
-    default only when those fill 8 rounds of the chip)."""
+    groups, ragged last n-tiles; the paired launches run their weight gradients in persistent workgroups and the
+    gate/up launch claims its last tiles by ticket (by default only when those fill 8 rounds of the chip)."""
     run_small_in_child("pipelined tile forced", PCMOE_GEMM_TILES=",".join(f"{k}=256x256w4" for k in range(6)),
                        PCMOE_DYN="2")
+
+
+@pytest.mark.timeout(400)
+def test_layer_small_pipelined_tile_ticket_tails():
+    """As above, with the pipelined paired launches' weight gradients on ticket-claimed tails instead of persistent
+    workgroups (PCMOE_PERSIST=0)."""
+    run_small_in_child("pipelined tile, ticket tails", PCMOE_GEMM_TILES=",".join(f"{k}=256x256w4" for k in range(6)),
+                       PCMOE_DYN="2", PCMOE_PERSIST="0")
 
 
 @pytest.mark.timeout(400)
