@@ -1084,8 +1084,14 @@ static int tile_shape(int kind, const moe_desc& d) {
   // The pipelined 4-wavefront tile pays off on long K loops only: its prologue and epilogue (one wavefront per
   // SIMD, each storing four times the outputs of a 16-wavefront tile's wavefront) are amortised over K. Measured:
   // 1.6% faster per layer step at d_model = 4096 (the dX + dW_gate|up pair 3.4%), equal at d_model = 2048 with
-  // 64 experts, 3% slower for a 16-expert shard at d_model = 2048 and 7% slower at d_model = 1024.
-  return d.d_model >= 4096 ? T256x256w4 : T256x256w16;
+  // 64 experts, 3% slower for a 16-expert shard at d_model = 2048 and 7% slower at d_model = 1024. With persistent
+  // weight-gradient workgroups, the dX + dW_gate|up pair also gains where its dX grid fills 8 rounds of the chip
+  // (d_model = 2048 with 64 experts: 6%), while the other kinds there stay faster on the 16-wavefront tile.
+  if (d.d_model >= 4096) return T256x256w4;
+  if ((kind == BWD_DX || kind == WG_GU) && d.d_model % 256 == 0 &&
+      mtile_bound2(d, 256) * (d.d_model / 256) >= 8L * device_cus())
+    return T256x256w4;
+  return T256x256w16;
 }
 
 // Upper bound on the m-tiles of the row-ragged kinds (per-expert counts stay on the device).
