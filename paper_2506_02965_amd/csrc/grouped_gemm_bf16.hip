@@ -558,8 +558,28 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
     }
     return;
   }
+  // The SwiGLU adjoint (BWD_DH) reads the saved G|U of its outputs. The pipelined tile's wavefronts have four times
+  // the outputs of a 16-wavefront tile's, so there the loads of the next part are issued before this part is
+  // staged and computed (two register buffers), and their latency is paid about once per tile instead of per part.
+  constexpr int GU_IT = C::PART_ROWS * CPRW / 64;  // output chunks per lane and part
+  constexpr bool GU_AHEAD = KIND == BWD_DH && C::PIPE;
+  Chunk gbuf[GU_AHEAD ? 2 : 1][GU_IT], ubuf[GU_AHEAD ? 2 : 1][GU_IT];
+  const auto load_gu = [&](int part, Chunk (&gch)[GU_IT], Chunk (&uch)[GU_IT]) {
+#pragma unroll
+    for (int it = 0; it < GU_IT; ++it) {
+      const int qq = lane + 64 * it, rr = qq / CPRW, cc = (qq % CPRW) * 8;
+      const int m = min(m0 + wm * C::WTM + part * C::PART_ROWS + rr, rows - 1);  // rows past the group: unused
+      const char* gu = (const char*)p.gu + ((rs + m) * 2 * f + n0 + wn * OUT_W + cc) * ES;
+      gch[it] = ld_chunk(gu);
+      uch[it] = ld_chunk(gu + (size_t)f * ES);
+    }
+  };
+  if constexpr (GU_AHEAD) load_gu(0, gbuf[0], ubuf[0]);
 #pragma unroll
   for (int part = 0; part < C::FM / FPP; ++part) {
+    if constexpr (GU_AHEAD) {
+      if (part + 1 < C::FM / FPP) load_gu(part + 1, gbuf[(part + 1) & 1], ubuf[(part + 1) & 1]);
+    }
     if constexpr (C::PIPE) {
       // The pipelined tile multiplies B by A: lane (q, li) of block (i, j) holds row 16 i + li, columns 16 j + 4 q ..
       // 16 j + 4 q + 3, staged with one 16-byte write.
@@ -579,19 +599,12 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's staging writes are done
     __builtin_amdgcn_wave_barrier();
     if constexpr (KIND == BWD_DH) {
-      // The SwiGLU adjoint reads the saved G|U of its outputs: the loads of the whole part are issued
-      // together, so their latency is paid once per part rather than once per chunk.
-      constexpr int IT = C::PART_ROWS * CPRW / 64;  // output chunks per lane and part
+      // (the 16-wavefront tiles load the whole part's G|U together here, so their latency is paid once per part)
+      constexpr int IT = GU_IT;
       static_assert(IT * 64 == C::PART_ROWS * CPRW, "epilogue chunks per lane");
-      Chunk gch[IT], uch[IT];
-#pragma unroll
-      for (int it = 0; it < IT; ++it) {
-        const int qq = lane + 64 * it, rr = qq / CPRW, cc = (qq % CPRW) * 8;
-        const int m = min(m0 + wm * C::WTM + part * C::PART_ROWS + rr, rows - 1);  // rows past the group: unused
-        const char* gu = (const char*)p.gu + ((rs + m) * 2 * f + n0 + wn * OUT_W + cc) * ES;
-        gch[it] = ld_chunk(gu);
-        uch[it] = ld_chunk(gu + (size_t)f * ES);
-      }
+      Chunk(&gch)[IT] = gbuf[GU_AHEAD ? (part & 1) : 0];
+      Chunk(&uch)[IT] = ubuf[GU_AHEAD ? (part & 1) : 0];
+      if constexpr (!GU_AHEAD) load_gu(part, gch, uch);
 #pragma unroll
       for (int it = 0; it < IT; ++it) {
         const int qq = lane + 64 * it, rr = qq / CPRW, cc = (qq % CPRW) * 8;
