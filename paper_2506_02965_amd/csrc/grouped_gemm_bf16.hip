@@ -14,10 +14,14 @@
 //     wavefronts for a single-round down projection, 128 x 128 tiles with 4 when a side is not a multiple
 //     of 256; for d_model >= 4096, a software-pipelined 256 x 256 tile with 4 wavefronts (one per SIMD,
 //     128 x 128 each, accumulators in AGPRs, 32-deep K-tiles in a 4-stage ring) for every contraction but
-//     the down projection; fp32 accumulators, per-wave epilogue staged through LDS in fp32 and written as
+//     the down projection (and for dX + dW_gate|up wherever the dX grid fills 8 rounds of the chip); fp32
+//     accumulators, per-wave epilogue staged through LDS (fp32, or bf16 for plain stores) and written as
 //     16-byte chunks (SwiGLU and its adjoint fused);
 //   * tiles decoded on the device from a plan of m-tile prefixes (grouped_gemm.h); independent
-//     contractions of the backward share one launch (gemm_bf16_pair_kernel).
+//     contractions of the backward share one launch (gemm_bf16_pair_kernel);
+//   * large launches claim their last eighth of tiles by ticket, so XCDs that run ahead take more of them;
+//     the pipelined tile's weight gradients run in persistent workgroups (wg_persistent) that overlap each
+//     finished tile's epilogue with the next tile's first loads.
 #include "grouped_gemm.h"
 
 #include <algorithm>
