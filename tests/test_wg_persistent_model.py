@@ -184,3 +184,39 @@ def test_epilogue_stores_in_bounds_and_cover_once():
                 covered[buf][off // 16] += 1
         for buf, c in covered.items():
             assert (c == 1).all(), (kind, buf, int(c.min()), int(c.max()))
+
+
+def ticket_split(tiles, cus=256, forced=False, pair=True):
+    """The ticket-claimed tail of a launch (run_pair2 / run2): returns (static count, dynamic count, ticket-taking
+    workgroups); tiles are tiles_b for a pair, the grid (a multiple of 8) for a single launch."""
+    if pair:
+        if forced:
+            dyn = min(tiles, max(tiles // 64 * 8, 8))
+        elif tiles >= 8 * cus:
+            dyn = tiles // 64 * 8
+        else:
+            dyn = 0
+    else:
+        grid = tiles
+        if forced:
+            dyn = min(grid, max(grid // 64 * 8, 8))
+        elif grid >= 8 * cus:
+            dyn = grid // 64 * 8
+        else:
+            dyn = 0
+    return tiles - dyn, dyn, (dyn + 256 if dyn > 0 else 0)
+
+
+def test_ticket_tails_cover_every_tile_once():
+    # static workgroups take indices [0, static); ticket t < dyn takes static + t; the rest take nothing
+    for tiles in [1, 7, 8, 63, 64, 100, 2047, 2048, 7168, 14336, 7504]:
+        for forced in (False, True):
+            for pair in (False, True):
+                n = tiles if pair else (tiles + 7) // 8 * 8
+                static, dyn, wgs = ticket_split(n, forced=forced, pair=pair)
+                assert 0 <= dyn <= n and static + dyn == n and (dyn == 0 or wgs >= dyn)
+                rng = random.Random(tiles)
+                tickets = list(range(wgs))
+                rng.shuffle(tickets)  # any order of arrival
+                done = list(range(static)) + [static + t for t in tickets if t < dyn]
+                assert sorted(done) == list(range(n))
