@@ -95,6 +95,11 @@ def small_cases():
     C["pipelined_d4096_empty_experts"] = (LayerConfig("p4e", T=512, d=4096, f=256, E=8, k=2, bias="forced_empty",
                                                       seed=33), two_empty)
 
+    # d_model = 4096 with enough weight-gradient tiles (9 groups x 32 x 16 and 9 x 16 x 16) that both backward
+    # launches run their weight gradients in persistent workgroups by default, beside a shared expert
+    C["pipelined_persistent_default"] = (LayerConfig("pp", T=1024, d=4096, f=4096, E=8, k=2, n_shared=1, seed=34),
+                                         None)
+
     def zero_router(inp):
         inp.w_router[:] = 0
     C["ties_all_equal"] = (LayerConfig("z", T=256, d=128, f=128, E=8, k=3, seed=21), zero_router)
