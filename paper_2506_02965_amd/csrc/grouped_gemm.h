@@ -30,6 +30,8 @@ struct GemmArgs {
   int wg_interleave;          // weight gradients: with near-equal groups (order[G] = 1), tile L belongs to group
                               // order[L % G] (round-robin over groups)
   int* tickets;               // single-contraction bf16 launches: a zeroed counter for ticket-claimed tiles, or null
+  int tail_split;             // with mt_tail: split each tail tile into up to this many column windows (0 or 1: none)
+  int tail_cus;               // ... as long as all the windows fit this many workgroups (the chip's CUs)
 };
 
 template <int KIND> struct KindTraits;
@@ -59,6 +61,7 @@ __device__ __forceinline__ int wave_pick(const int (&v)[NS], int i) {
 struct TileIdx {
   int g, mt, nt;
   int row0, rows;  // the group's first row in its source and its row count
+  int sub, nsub;   // column window sub of nsub equal windows: a split tail tile's (nsub = tail_split), else 0 of 1
 };
 // The plan arrays a tile decode reads, spread over the wavefront (entry 64 s + lane in slot s).
 struct DecodeArrays {
@@ -119,6 +122,14 @@ __device__ __forceinline__ bool decode_with(const GemmArgs& p, int bid, const De
   // turn); they are dealt round-robin over the XCDs so that the long ones spread out.
   int L;
   bool tail = false;
+  // Split tail tiles: the largest power of two up to tail_split whose windows of all tail tiles fit tail_cus
+  // workgroups (a split tail tile takes about as long as a whole one, so more windows than CUs cost a round).
+  int ts = 1;
+  if (split && p.tail_split > 1) {
+    const int ptiles = wave_pick(tl, G) * p.n_tiles;
+    ts = p.tail_split;
+    while (ts > 1 && ptiles * ts > p.tail_cus) ts >>= 1;
+  }
   if (RAGGED) {
     // XCD x = bid % 8 takes the run [x * q + min(x, r), ...) of q or q + 1 tiles (total = 8 q + r) of each
     // segment: the counts differ by at most one between XCDs
@@ -129,7 +140,7 @@ __device__ __forceinline__ bool decode_with(const GemmArgs& p, int bid, const De
       L = x * q + min(x, r) + lb;
     } else {
       if (!split) return false;
-      const int ptot = wave_pick(tl, G) * p.n_tiles;
+      const int ptot = wave_pick(tl, G) * p.n_tiles * ts;
       const int qt = ptot >> 3, rt = ptot & 7;
       const int lt = lb - cnt;
       if (lt >= qt + (x < rt ? 1 : 0)) return false;
@@ -141,10 +152,12 @@ __device__ __forceinline__ bool decode_with(const GemmArgs& p, int bid, const De
   }
   if (!tail && L >= total) return false;
   int l, n_mt;
+  t.sub = 0;
+  t.nsub = 1;
   if (tail) {
-    // the group of tail tile L / n_tiles: largest g whose tail prefix is <= it (groups without a tail share
-    // their successor's prefix and are passed over)
-    const int tix = L / p.n_tiles;
+    // the group of tail tile L / (n_tiles * ts): largest g whose tail prefix is <= it (groups without a tail share
+    // their successor's prefix and are passed over); a split tail tile's windows are consecutive
+    const int tix = L / (p.n_tiles * ts);
     int g = 0;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
@@ -158,7 +171,10 @@ __device__ __forceinline__ bool decode_with(const GemmArgs& p, int bid, const De
     const bool routed_t = g < p.Eloc;
     t.row0 = routed_t ? wave_pick(off, g) : 0;
     t.rows = routed_t ? wave_pick(off, g + 1) - t.row0 : p.T;
-    t.nt = __builtin_amdgcn_readfirstlane(L - tix * p.n_tiles);
+    const int rem = L - tix * p.n_tiles * ts;
+    t.nt = __builtin_amdgcn_readfirstlane(rem / ts);
+    t.sub = __builtin_amdgcn_readfirstlane(rem - (rem / ts) * ts);
+    t.nsub = ts;
     t.mt = __builtin_amdgcn_readfirstlane(wave_pick(pre, g + 1) - wave_pick(pre, g));  // after the group's others
     return true;
   }

@@ -200,6 +200,11 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
   const int row0 = ti.row0, rows = ti.rows;
   const size_t rs = routed ? (size_t)row0 : (size_t)p.rows_cap + (size_t)(g - p.Eloc) * p.T;
   const int m0 = ti.mt * BM, n0 = ti.nt * BN;
+  // A split tail tile of the down projection (two-stage ring) computes only the columns of its window: the other
+  // wavefront columns skip their MFMAs and stores, and the B loads of the rows outside the window are not issued.
+  // Every other tile is one window of the whole tile.
+  const int nsub = (KIND == FWD_DOWN && STAGES == 2) ? ti.nsub : 1;
+  const int wlo = ti.sub * (BN / nsub), whi = wlo + BN / nsub;
   int K;
   if (KIND == FWD_GU || KIND == BWD_DH) K = d;
   else if (KIND == FWD_DOWN) K = f;
@@ -295,6 +300,8 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
           voff + (KT::a_kc ? k0 * ES : k0 * a_ld));
   };
   const auto load_b = [&](int kt, int stage, int jj, int voff, bool up) {
+    // (a split tail tile: every row of instruction jj lies outside the window or none does; the waits are vmcnt(0))
+    if (KIND == FWD_DOWN && STAGES == 2 && (C::RPI * jj < wlo || C::RPI * jj >= whi)) return;
     const int k0 = kt * BK;
     const uint32_t dst = lds_base + stage * C::STAGE_BYTES + C::A_BYTES + jj * 1024 + pad(jj, KT::b_kc, MKP_B);
     if (KIND == BWD_DX) {
@@ -318,7 +325,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
   // 128 and a wave's columns a 64-aligned block, so each wave's columns are all inside or all past N). Its
   // B loads past N read neighbouring rows or zeros through the buffer range check: finite values that reach
   // only the columns past N, which are neither computed nor stored.
-  const bool wave_cols = n0 + wn * C::WTN < p.n_extent;  // wave-uniform
+  const bool wave_cols = n0 + wn * C::WTN < p.n_extent && wn * C::WTN >= wlo && wn * C::WTN < whi;  // wave-uniform
 
   // Operand fragments of MFMA k-step kk (32 deep) of the K-tile whose stage starts at As (A) / Bs (B).
   // K-contiguous fragments: row 16 * i + li of the wave's rows; the swizzle sees only li, and fragment i sits FRAG
@@ -453,36 +460,53 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, int bid, char* smem
     }
     Chunk fa[2][C::FM], fb[2][C::FN];
     read_frags(smem, smem + C::A_BYTES, 0, fa[0], fb[0]);
-    // the step of K-tile kt with its fragments in register set S
-    const auto step = [&](int kt, auto set) {
+    // The step of K-tile kt with its fragments in register set S, for the first FMA row blocks of the wavefront:
+    // all 8, or 4 when its rows past the first 64 all lie past the group's end (a group's last m-tile; the MFMAs
+    // of the empty blocks would leave their accumulators at zero, and the epilogue skips those rows). The half
+    // step spreads the same fragment reads of its blocks and the same 8 direct loads over its 24 MFMAs after the
+    // barrier, so the waits and barriers are those of the full step.
+    const auto step = [&](int kt, auto set, auto blocks) {
       constexpr int S = decltype(set)::value;
+      constexpr int FMA = decltype(blocks)::value;
+      constexpr int NM = FMA * C::FN;                // MFMAs of the step
+      constexpr int MB = NM / 4;                     // MFMAs before the wait and barrier
+      constexpr int RS = (NM - MB) / (FMA + C::FN);  // MFMAs per fragment read: 3, or 2 for the half step
+      constexpr int LS = (NM - MB) / 8;              // MFMAs per direct load: 6, or 3
+      static_assert(RS * (FMA + C::FN) == NM - MB && LS * 8 == NM - MB, "pipelined step schedule");
       const char* As = smem + ((kt + 1) & 3) * C::STAGE_BYTES;
 #pragma unroll
-      for (int i = 0; i < C::FM; ++i) {
+      for (int i = 0; i < FMA; ++i) {
 #pragma unroll
         for (int j = 0; j < C::FN; ++j) {
           const int m = i * C::FN + j;
-          if (m == 16) {
+          if (m == MB) {
             wait_vmcnt<16>();  // K-tile kt + 1 has landed (kt + 2 and kt + 3 may be in flight)
             barrier();
           }
           mfma_bf16_agpr(acc[i][j], fb[S][j], fa[S][i]);  // transposed block: 4 consecutive columns per lane
-          if (m >= 16) {
-            const int r = m - 16;  // 0..47: a read after every third MFMA, a load after every sixth
-            if (r % 3 == 0) {
-              const int t = r / 3;  // fa[0], fb[0..7], fa[1..7]
+          if (m >= MB) {
+            const int r = m - MB;  // a read after every RS-th MFMA, a load after every LS-th
+            if (r % RS == 0) {
+              const int t = r / RS;  // fa[0], fb[0..7], fa[1..FMA-1]
               if (t == 0) fa[S ^ 1][0] = frag_a(As, 0, 0);
-              else if (t <= 8) fb[S ^ 1][t - 1] = frag_b(As + C::A_BYTES, 0, t - 1);
-              else fa[S ^ 1][t - 8] = frag_a(As, 0, t - 8);
+              else if (t <= C::FN) fb[S ^ 1][t - 1] = frag_b(As + C::A_BYTES, 0, t - 1);
+              else fa[S ^ 1][t - C::FN] = frag_a(As, 0, t - C::FN);
             }
-            if (r % 6 == 2) load_one(kt + 4, r / 6);
+            if (r % LS == LS / 3) load_one(kt + 4, r / LS);
           }
         }
       }
     };
-    for (int kt = 0; kt < KTN2; kt += 2) {
-      step(kt, std::integral_constant<int, 0>{});
-      step(kt + 1, std::integral_constant<int, 1>{});
+    if (KT::ragged_m && m0 + wm * C::WTM + C::WTM / 2 >= rows) {  // wave-uniform
+      for (int kt = 0; kt < KTN2; kt += 2) {
+        step(kt, std::integral_constant<int, 0>{}, std::integral_constant<int, C::FM / 2>{});
+        step(kt + 1, std::integral_constant<int, 1>{}, std::integral_constant<int, C::FM / 2>{});
+      }
+    } else {
+      for (int kt = 0; kt < KTN2; kt += 2) {
+        step(kt, std::integral_constant<int, 0>{}, std::integral_constant<int, C::FM>{});
+        step(kt + 1, std::integral_constant<int, 1>{}, std::integral_constant<int, C::FM>{});
+      }
     }
     wait_vmcnt<0>();  // the zero-filling loads past the last K-tile land before the epilogue reuses the LDS
     asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");  // the last MFMAs' results are ready to read
@@ -1208,6 +1232,15 @@ struct Prep {
   long tiles;
 };
 
+// Column windows per tail tile of the down projection: 4 (PCMOE_TAIL_SPLIT=1, 2 or 4 overrides).
+static int tail_split_windows() {
+  static const int ts = [] {
+    const char* env = getenv("PCMOE_TAIL_SPLIT");
+    return env && (env[0] == '1' || env[0] == '2' || env[0] == '4') ? env[0] - '0' : 4;
+  }();
+  return ts;
+}
+
 // Ragged-M contraction with n_cols output columns in the tile grid (FWD_GU: gate and up columns). tails_last:
 // split off the tails even when the grid is one round (a paired launch, where it shares the chip).
 template <int KIND>
@@ -1223,7 +1256,18 @@ static Prep prep_ragged(const moe_desc& d, GemmArgs a, const Plan& pl, int n_col
   const bool split = bm == 256 && (tails_last || bound > device_cus());
   a.mt_prefix = bm == 128 ? pl.pre128 : bm == 192 ? pl.pre192 : split ? pl.body256 : pl.pre256;
   a.mt_tail = split ? pl.tail256 : nullptr;
-  return Prep{sh, a, bound + (split ? 16 : 0)};
+  // A down projection of a few rounds runs its tails (at most half a tile of rows each) in a last, partial round,
+  // where each tail tile still loads its whole B panel and most CUs idle. Split into column windows (one per
+  // workgroup, consecutive in the tail segment), the tails load a window's B rows each and spread over those CUs;
+  // the decode takes fewer windows per tile when those of all the tails would not fit the CUs. Each group has at
+  // most one tail m-tile: the windows add at most (tail_split - 1) * G * n_tiles workgroups.
+  long extra = 0;
+  if (KIND == FWD_DOWN && split && sh == T256x256w16 && bound <= 8L * device_cus()) {
+    a.tail_split = tail_split_windows();
+    a.tail_cus = device_cus();
+    extra = (long)(a.tail_split - 1) * (d.local_count + d.n_shared) * a.n_tiles;
+  }
+  return Prep{sh, a, bound + (split ? 16 : 0) + extra};
 }
 // Weight gradient: an M x N output per group, K = the group's rows.
 template <int KIND>

@@ -99,6 +99,9 @@ def small_cases():
     # launches run their weight gradients in persistent workgroups by default, beside a shared expert
     C["pipelined_persistent_default"] = (LayerConfig("pp", T=1024, d=4096, f=4096, E=8, k=2, n_shared=1, seed=34),
                                          None)
+    # a down projection of 384 tiles of 256 x 256 (one and a half rounds of the chip) and three tail m-tiles of 22,
+    # 33 and 50 rows: each of the 24 tail tiles runs as four 64-column windows
+    C["down_tail_split"] = (LayerConfig("dts", T=4096, d=2048, f=512, E=8, k=2, n_shared=1, seed=35), None)
 
     def zero_router(inp):
         inp.w_router[:] = 0
