@@ -21,7 +21,10 @@
 //     contractions of the backward share one launch (gemm_bf16_pair_kernel);
 //   * large launches claim their last eighth of tiles by ticket, so XCDs that run ahead take more of them;
 //     the pipelined tile's weight gradients run in persistent workgroups (wg_persistent) that overlap each
-//     finished tile's epilogue with the next tile's first loads.
+//     finished tile's epilogue with the next tile's first loads;
+//   * a group's last m-tile with at most half a tile of rows (a tail) still loads its whole B panel: on the
+//     pipelined tile its wavefronts with at most 64 rows issue half the MFMAs, and a down projection of a few
+//     rounds splits its tail tiles into column windows that spread over the idle CUs of its last round.
 #include "grouped_gemm.h"
 
 #include <algorithm>
