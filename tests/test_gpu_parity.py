@@ -102,6 +102,9 @@ def small_cases():
     # a down projection of 384 tiles of 256 x 256 (one and a half rounds of the chip) and three tail m-tiles of 22,
     # 33 and 50 rows: each of the 24 tail tiles runs as four 64-column windows
     C["down_tail_split"] = (LayerConfig("dts", T=4096, d=2048, f=512, E=8, k=2, n_shared=1, seed=35), None)
+    # 13 tail m-tiles (1 to 37 rows) over 8 n-tiles: four windows each would not fit the chip's 256 CUs, so the
+    # decode takes two per tail tile
+    C["down_tail_split_fewer_windows"] = (LayerConfig("dtw", T=4096, d=2048, f=512, E=32, k=4, seed=37), None)
 
     def zero_router(inp):
         inp.w_router[:] = 0
