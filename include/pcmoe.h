@@ -142,8 +142,9 @@ moe_status moe_permute_noalloc(const moe_desc* desc, const int32_t* topk_idx, co
  *   w_up    [local_count + n_shared, f, d] dtype
  *   w_down  [local_count + n_shared, d, f] dtype
  *   y_perm  [R, d] dtype out (row space above)
- *   saved   MOE_WS_FFN_SAVED bytes out: G, U, H and the grouped-GEMM tile plan for the backward, and a tile
- *           counter of the gate/up launch (opaque; calls that overlap on the GPU need their own)
+ *   saved   MOE_WS_FFN_SAVED bytes out: G, U, H and the grouped-GEMM tile plan for the backward, and the tile
+ *           counters of the gate/up and down-projection launches (opaque; calls that overlap on the GPU need their
+ *           own)
  *   ws      MOE_WS_FFN_FWD bytes of scratch (currently 0: ws may be NULL)
  */
 moe_status moe_expert_ffn_fwd(const moe_desc* desc, const void* x, const void* x_perm, const int32_t* offsets,

@@ -220,12 +220,13 @@ __device__ __forceinline__ bool decode_with(const GemmArgs& p, int bid, const De
 // pre2 = m-tile prefixes for bm0-, bm1- and bm2-row tiles; for bm1-row tiles also body1 = prefix of the m-tiles
 // other than the tails and tail1 = prefix of the tails (a last m-tile holding at most bm1 / 2 rows); order =
 // groups by decreasing row count (ties by index), and order[G] = 1 when all groups' row counts lie within 25% of
-// the largest (0 otherwise).
+// the largest (0 otherwise). It also sets zero[0 .. nzero) to 0 (the tile counters of the launches that follow).
 __global__ __launch_bounds__(512) void mtile_prefix_kernel(const int32_t* __restrict__ offsets, int Eloc, int S,
                                                            int Tn, int bm0, int bm1, int bm2,
                                                            int32_t* __restrict__ pre0, int32_t* __restrict__ pre1,
                                                            int32_t* __restrict__ body1, int32_t* __restrict__ tail1,
-                                                           int32_t* __restrict__ pre2, int32_t* __restrict__ order);
+                                                           int32_t* __restrict__ pre2, int32_t* __restrict__ order,
+                                                           int32_t* __restrict__ zero, int nzero);
 
 // fp32 path (generic LDS-tiled MFMA 16x16x4 kernel)
 hipError_t ffn_fwd_f32(const moe_desc& d, const void* x, const void* xp, const int32_t* offsets, const void* wg,

@@ -1181,11 +1181,13 @@ static Plan plan_at(const moe_desc& d, void* where) {
   pl.pre192 = (int32_t*)((char*)where + 5 * plan_part(d));
   return pl;
 }
-static Plan plan(const moe_desc& d, const int32_t* offsets, void* where, hipStream_t s) {
+// (zero, nzero: counters the plan kernel also clears, for the launches that follow it)
+static Plan plan(const moe_desc& d, const int32_t* offsets, void* where, hipStream_t s, int32_t* zero = nullptr,
+                 int nzero = 0) {
   Plan pl = plan_at(d, where);
   KernelTimer kt("ffn_plan", s);
   hipLaunchKernelGGL(mtile_prefix_kernel, dim3(1), dim3(512), 0, s, offsets, d.local_count, d.n_shared, d.T, 128, 256,
-                     192, pl.pre128, pl.pre256, pl.body256, pl.tail256, pl.pre192, pl.order);
+                     192, pl.pre128, pl.pre256, pl.body256, pl.tail256, pl.pre192, pl.order, zero, nzero);
   return pl;
 }
 
@@ -1327,7 +1329,9 @@ static hipError_t run_pair(const Prep& A, const Prep& B, int* tickets, hipStream
 
 hipError_t launch_ffn_fwd(const moe_desc& d, const void* x, const void* xp, const int32_t* offsets, const void* wg,
                           const void* wu, const void* wd, void* yp, void* saved, void*, hipStream_t s) {
-  Plan pl = plan(d, offsets, (char*)saved + saved_plan_offset(d), s);
+  // the gate/up and down-projection tile counters (after the plan in the saved buffer), cleared by the plan kernel
+  int* tickets = (int*)((char*)saved + saved_plan_offset(d) + align256(plan_bytes(d)));
+  Plan pl = plan(d, offsets, (char*)saved + saved_plan_offset(d), s, tickets, 2);
   if (d.dtype != MOE_BF16) return ffn_fwd_f32(d, x, xp, offsets, wg, wu, wd, yp, saved, pl.pre128, s);
   const size_t R = (size_t)rows_total(d);
   GemmArgs a = args_for(d, offsets);
@@ -1338,10 +1342,8 @@ hipError_t launch_ffn_fwd(const moe_desc& d, const void* x, const void* xp, cons
   hipError_t e;
   GemmArgs a_gu = a, a_down = a;
   if (dynamic_tiles()) {
-    a_gu.tickets = (int*)((char*)saved + saved_plan_offset(d) + align256(plan_bytes(d)));
-    a_down.tickets = a_gu.tickets + 1;
-    hipLaunchKernelGGL(zero_tickets_kernel, dim3(1), dim3(64), 0, s, a_gu.tickets, 2);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    a_gu.tickets = tickets;
+    a_down.tickets = tickets + 1;
   }
   if ((e = run<FWD_GU>(prep_ragged<FWD_GU>(d, a_gu, pl, 2 * d.d_ff), s)) != hipSuccess) return e;
   return run<FWD_DOWN>(prep_ragged<FWD_DOWN>(d, a_down, pl, d.d_model), s);

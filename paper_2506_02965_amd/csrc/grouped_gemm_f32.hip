@@ -363,10 +363,12 @@ __global__ __launch_bounds__(512) void mtile_prefix_kernel(const int32_t* __rest
                                                            int Tn, int bm0, int bm1, int bm2,
                                                            int32_t* __restrict__ pre0, int32_t* __restrict__ pre1,
                                                            int32_t* __restrict__ body1, int32_t* __restrict__ tail1,
-                                                           int32_t* __restrict__ pre2, int32_t* __restrict__ order) {
+                                                           int32_t* __restrict__ pre2, int32_t* __restrict__ order,
+                                                           int32_t* __restrict__ zero, int nzero) {
   __shared__ int buf[5][2][512];
   __shared__ int rows_s[512];
   const int g = threadIdx.x;
+  if (zero && g < nzero) zero[g] = 0;
   const int G = Eloc + S;
   int rows = 0;
   if (g < Eloc) rows = offsets[g + 1] - offsets[g];
