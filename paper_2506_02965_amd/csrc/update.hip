@@ -1,11 +1,13 @@
 // Expert parameter update (the step that closes the host's expert pass in Alg. 6): SGD or AdamW with decoupled weight
 // decay, elementwise in fp32 over the hosted and shared experts' w_gate, w_up and w_down.
-// Bandwidth-bound: each thread updates 8 consecutive parameters with 16-byte vector accesses.
+// Bandwidth-bound: each wavefront updates 512 consecutive parameters with contiguous vector accesses.
 #include "pcmoe_internal.h"
 
 #include <math.h>
 
 namespace pcmoe {
+
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 struct UpdateArgs {
   void* w[3];             // w_gate, w_up, w_down (dtype)
@@ -20,56 +22,72 @@ struct UpdateArgs {
   float decay;            // 1 - lr * wd
 };
 
-// One thread per group of 8 consecutive parameters (measured faster than a grid-stride loop over a
-// capped grid).
+// Each wavefront updates a block of 512 consecutive parameters of one tensor; lane l takes parameters 4l .. 4l + 3
+// and 256 + 4l .. 256 + 4l + 3 of the block, so that every access of the wavefront (8 bytes per lane of a bf16
+// tensor, 16 bytes of an fp32 one) covers a contiguous range. Every tensor holds a multiple of 16,384 parameters.
+// The accesses are non-temporal: each byte is read or written once per step, and the state of a large layer is
+// many times the last-level cache (measured 4-6% faster than plain accesses).
+template <typename T>
+__device__ __forceinline__ void ld4(const T* p, float (&v)[4]);
+template <>
+__device__ __forceinline__ void ld4<float>(const float* p, float (&v)[4]) {
+  const floatx4 x = __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(p));
+  v[0] = x[0]; v[1] = x[1]; v[2] = x[2]; v[3] = x[3];
+}
+template <>
+__device__ __forceinline__ void ld4<bf16>(const bf16* p, float (&v)[4]) {
+  const u32x2 x = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
+  v[0] = __uint_as_float(x[0] << 16); v[1] = __uint_as_float(x[0] & 0xffff0000u);
+  v[2] = __uint_as_float(x[1] << 16); v[3] = __uint_as_float(x[1] & 0xffff0000u);
+}
+template <typename T>
+__device__ __forceinline__ void st4(T* p, const float (&v)[4]);
+template <>
+__device__ __forceinline__ void st4<float>(float* p, const float (&v)[4]) {
+  __builtin_nontemporal_store(floatx4{v[0], v[1], v[2], v[3]}, reinterpret_cast<floatx4*>(p));
+}
+template <>
+__device__ __forceinline__ void st4<bf16>(bf16* p, const float (&v)[4]) {
+  __builtin_nontemporal_store(u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])}, reinterpret_cast<u32x2*>(p));
+}
+
 template <typename T, bool ADAM, bool MASTER>
 __global__ __launch_bounds__(256) void expert_update_kernel(UpdateArgs a) {
-  constexpr int EP = EPC<T>::value;  // elements per 16-byte chunk of the dtype
-  const long per = a.n / 8;          // 8-parameter groups per tensor
-  const long q = blockIdx.x * (long)blockDim.x + threadIdx.x;
-  if (q < 3 * per) {
-    const int seg = (int)(q / per);
-    const long e0 = (q - seg * per) * 8;  // first parameter within the tensor
-    const long f0 = seg * a.n + e0;       // and within the fp32 state arrays
-    T* w = reinterpret_cast<T*>(a.w[seg]) + e0;
-    const T* g = reinterpret_cast<const T*>(a.g[seg]) + e0;
-    float p[8], gr[8];
+  const long blocks = a.n / 512;  // 512-parameter blocks per tensor
+  const long wv = (blockIdx.x * (long)blockDim.x + threadIdx.x) >> 6;
+  const int lane = threadIdx.x & 63;
+  if (wv >= 3 * blocks) return;
+  const int seg = (int)(wv / blocks);
+  const long b0 = (wv - seg * blocks) * 512;  // first parameter of the block within the tensor
+  T* w = reinterpret_cast<T*>(a.w[seg]) + b0;
+  const T* g = reinterpret_cast<const T*>(a.g[seg]) + b0;
+  const long f0 = seg * a.n + b0;  // the block within the fp32 state arrays
 #pragma unroll
-    for (int c = 0; c < 8 / EP; ++c) chunk_to_f<T>(ld_chunk(g + c * EP), gr + c * EP);
-    if (MASTER) {
-      chunk_to_f<float>(ld_chunk(a.master + f0), p);
-      chunk_to_f<float>(ld_chunk(a.master + f0 + 4), p + 4);
-    } else {
-#pragma unroll
-      for (int c = 0; c < 8 / EP; ++c) chunk_to_f<T>(ld_chunk(w + c * EP), p + c * EP);
-    }
+  for (int h = 0; h < 2; ++h) {
+    const int o = 256 * h + 4 * lane;
+    float p[4], gr[4];
+    ld4<T>(g + o, gr);
+    if (MASTER) ld4<float>(a.master + f0 + o, p);
+    else ld4<T>(w + o, p);
     if (ADAM) {
-      float mm[8], vv[8];
-      chunk_to_f<float>(ld_chunk(a.m + f0), mm);
-      chunk_to_f<float>(ld_chunk(a.m + f0 + 4), mm + 4);
-      chunk_to_f<float>(ld_chunk(a.v + f0), vv);
-      chunk_to_f<float>(ld_chunk(a.v + f0 + 4), vv + 4);
+      float mm[4], vv[4];
+      ld4<float>(a.m + f0 + o, mm);
+      ld4<float>(a.v + f0 + o, vv);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
+      for (int i = 0; i < 4; ++i) {
         p[i] *= a.decay;
         mm[i] = a.beta1 * mm[i] + (1.f - a.beta1) * gr[i];
         vv[i] = a.beta2 * vv[i] + (1.f - a.beta2) * gr[i] * gr[i];
         p[i] -= a.step_size * mm[i] / (sqrtf(vv[i]) * a.inv_sqrt_bc2 + a.eps);
       }
-      st_chunk(a.m + f0, f_to_chunk<float>(mm));
-      st_chunk(a.m + f0 + 4, f_to_chunk<float>(mm + 4));
-      st_chunk(a.v + f0, f_to_chunk<float>(vv));
-      st_chunk(a.v + f0 + 4, f_to_chunk<float>(vv + 4));
+      st4<float>(a.m + f0 + o, mm);
+      st4<float>(a.v + f0 + o, vv);
     } else {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) p[i] -= a.lr * (gr[i] + a.wd * p[i]);
+      for (int i = 0; i < 4; ++i) p[i] -= a.lr * (gr[i] + a.wd * p[i]);
     }
-    if (MASTER) {
-      st_chunk(a.master + f0, f_to_chunk<float>(p));
-      st_chunk(a.master + f0 + 4, f_to_chunk<float>(p + 4));
-    }
-#pragma unroll
-    for (int c = 0; c < 8 / EP; ++c) st_chunk(w + c * EP, f_to_chunk<T>(p + c * EP));
+    if (MASTER) st4<float>(a.master + f0 + o, p);
+    st4<T>(w + o, p);
   }
 }
 
@@ -87,8 +105,7 @@ hipError_t launch_expert_update(const moe_desc& d, const moe_opt& o, void* wg, v
   a.step_size = o.kind == MOE_OPT_ADAMW ? (float)((double)o.lr / bc1) : 0.f;
   a.inv_sqrt_bc2 = o.kind == MOE_OPT_ADAMW ? (float)(1.0 / sqrt(bc2)) : 0.f;
   a.decay = (float)(1.0 - (double)o.lr * (double)o.weight_decay);
-  const long groups = 3 * (a.n / 8);
-  const long blocks = (groups + 255) / 256;  // < 2^31 (checked by moe_expert_update)
+  const long blocks = 3 * (a.n / 512) / 4;  // four 512-parameter blocks per workgroup; < 2^31 (moe_expert_update)
   KernelTimer kt("expert_update", s);
 #define UPD(T, ADAM, MASTER) \
   hipLaunchKernelGGL((expert_update_kernel<T, ADAM, MASTER>), dim3((unsigned)blocks), dim3(256), 0, s, a)
