@@ -1307,6 +1307,14 @@ static bool pair_enabled() {
   return on;
 }
 
+// Whether run_pair below launches A and B together with B's last tiles claimed at run time (by ticket or by
+// persistent workgroups), that is whether it reads the tile counters it is given: the condition run_pair2 applies.
+static bool pair_claims(const Prep& A, const Prep& B) {
+  if (!pair_enabled() || A.sh != B.sh) return false;
+  if (A.sh != T256x256w16 && A.sh != T256x256w4 && A.sh != T128x128s2) return false;  // no paired kernel
+  return dynamic_tiles() == 2 || B.tiles >= 8L * device_cus();
+}
+
 // Independent contractions A and B (no operand of one is written by the other) in one launch when
 // they share a tile shape; A's workgroups come first.
 template <int KA, int KB>
@@ -1371,17 +1379,17 @@ hipError_t launch_ffn_bwd(const moe_desc& d, const void* x, const void* xp, cons
   a_wgu.out2 = dwu;
   a_dx.out = dxp;
   int* tickets = (int*)((char*)ws + align256(R * 2 * d.d_ff * es));
-  if (dynamic_tiles()) {
+  const Prep dh = prep_ragged<BWD_DH>(d, a, pl, d.d_ff), wd_ = prep_wgrad<WG_DOWN>(d, a_wd, pl, d.d_model, d.d_ff);
+  const Prep dx = prep_ragged<BWD_DX>(d, a_dx, pl, d.d_model, pair_enabled()),
+             wgu = prep_wgrad<WG_GU>(d, a_wgu, pl, 2 * d.d_ff, d.d_model);
+  // the counters are read only by paired launches that claim tiles at run time: cleared (one launch) only then
+  if (dynamic_tiles() && (pair_claims(dh, wd_) || pair_claims(dx, wgu))) {
     hipLaunchKernelGGL(zero_tickets_kernel, dim3(1), dim3(64), 0, s, tickets, 16);
     if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   }
-  hipError_t e = run_pair<BWD_DH, WG_DOWN>(prep_ragged<BWD_DH>(d, a, pl, d.d_ff),
-                                           prep_wgrad<WG_DOWN>(d, a_wd, pl, d.d_model, d.d_ff),
-                                           dynamic_tiles() ? tickets : nullptr, s, "gemm_bwd_dh+wgrad_down");
+  hipError_t e = run_pair<BWD_DH, WG_DOWN>(dh, wd_, dynamic_tiles() ? tickets : nullptr, s, "gemm_bwd_dh+wgrad_down");
   if (e != hipSuccess) return e;
-  return run_pair<BWD_DX, WG_GU>(prep_ragged<BWD_DX>(d, a_dx, pl, d.d_model, pair_enabled()),
-                                 prep_wgrad<WG_GU>(d, a_wgu, pl, 2 * d.d_ff, d.d_model),
-                                 dynamic_tiles() ? tickets + 8 : nullptr, s, "gemm_bwd_dx+wgrad_gate_up");
+  return run_pair<BWD_DX, WG_GU>(dx, wgu, dynamic_tiles() ? tickets + 8 : nullptr, s, "gemm_bwd_dx+wgrad_gate_up");
 }
 
 }  // namespace pcmoe
